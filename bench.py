@@ -1,0 +1,309 @@
+#!/usr/bin/env python3
+"""Benchmark of the distilled modal recurrence on one MI355X.
+
+One step = one pass of the whole hot path over one batch of the workload:
+prefill of the B x T prompt (all outputs + post-prompt state) followed by K
+decode steps (one lh_step launch per token, replayed from a HIP graph).
+Inputs are resident in HBM before the timed region starts.
+
+Prints ONE JSON line: decode tokens/s (B * K / decode time) as ``value``,
+prefill tokens/s, the decode kernel's roofline (HBM) and the prefill's
+(ALU), and the CPU oracle timed on a bounded sample of the same workload.
+
+    python bench.py [--steps K] [--warmup W] [--workload c3]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import re
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "decode tokens/s (B·steps/s) + HBM GB/s at D=2048,d=16; prefill tokens/s"
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E
+FP32_VALU_PEAK_TFLOPS = 157.3  # MI355X fp32 vector (with packed FP32 FMA)
+PROFILES = os.path.join(ROOT, "profiles")
+
+
+def parse():
+    p = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=20)
+    p.add_argument("--warmup", type=int, default=3)
+    p.add_argument("--workload", default="c3")
+    p.add_argument("--decode-launch", choices=["graph", "eager"], default="graph")
+    p.add_argument("--no-cpu-baseline", action="store_true",
+                   help="leave out the oracle timing (cpu_baseline is then null)")
+    p.add_argument("--cpu-rows", type=int, default=0,
+                   help="(b, c) rows of the oracle sample (0: sized for ~15 s)")
+    p.add_argument("--stream-pool", type=int, default=64,
+                   help="state buffers of the HBM-streaming decode measurement (0: skip)")
+    p.add_argument("--copy-calibration", action="store_true",
+                   help="run only a plain device copy of known size (counter calibration)")
+    return p.parse_args()
+
+
+def src_digest(*names):
+    h = hashlib.sha256()
+    for n in names:
+        with open(os.path.join(ROOT, "paper_2310_18780_amd", "csrc", n), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def counter_traffic(summary_name, digest):
+    """HBM bytes per launch from a committed rocprofv3 counter summary, if it
+    was taken on the current kernel source (else None)."""
+    path = os.path.join(PROFILES, summary_name)
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    m_src = re.search(r"^source_sha256_16:\s*([0-9a-f]+)", text, re.M)
+    m_b = re.search(r"^hbm_bytes_per_launch:\s*([0-9.eE+]+)", text, re.M)
+    if not m_src or not m_b or m_src.group(1) != digest:
+        return None
+    return float(m_b.group(1))
+
+
+def copy_calibration():
+    import torch
+
+    n = 256 << 20
+    a = torch.empty(n, dtype=torch.uint8, device="cuda").fill_(1)
+    b = torch.empty_like(a)
+    for _ in range(5):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_bytes": n, "launches": 5}))
+
+
+def make_device_inputs(w):
+    import numpy as np
+    import torch
+
+    import workloads
+
+    lam, R, h0 = workloads.make_params(w)
+    iot = torch.bfloat16 if w.io == "bf16" else torch.float32
+    u = torch.empty((w.B, w.T, w.D), dtype=iot, device="cuda")
+    ud = torch.empty((w.K, w.B, w.D), dtype=iot, device="cuda")
+    for b in range(w.B):
+        u[b].copy_(torch.from_numpy(workloads.prompt_row(w, b)))
+        ud[:, b].copy_(torch.from_numpy(workloads.decode_row(w, b)))
+    return dict(lam=torch.from_numpy(lam).cuda(), R=torch.from_numpy(R).cuda(),
+                h0=torch.from_numpy(h0).cuda(), u=u, ud=ud)
+
+
+def decode_bytes(w):
+    es = 2 if w.io == "bf16" else 4
+    return 16 * w.B * w.D * w.d + 2 * es * w.B * w.D + 16 * w.D * w.d + 4 * w.D
+
+
+def prefill_bytes(w):
+    es = 2 if w.io == "bf16" else 4
+    return 2 * es * w.B * w.T * w.D + 8 * w.B * w.D * w.d + 16 * w.D * w.d + 4 * w.D
+
+
+def prefill_flops(w):
+    return 12 * w.d * w.B * w.T * w.D + 2 * w.B * w.T * w.D
+
+
+def cpu_baseline(w, rows_wanted):
+    """The oracle (as it stands) on a bounded sample: complete rows (prompt
+    outputs, decode outputs, both states) of (b, c) pairs of the workload."""
+    import numpy as np
+
+    import oracle
+    import workloads
+
+    lam, R, h0 = workloads.make_params(w)
+    L = w.T + w.K
+    if rows_wanted <= 0:
+        # ~12 s: direct convolution costs L^2/2 multiply-adds per row at about
+        # 0.5e9 per core
+        rate = 0.5e9 * max(1, oracle.native_threads())
+        rows_wanted = int(max(64, min(w.B * w.D, 12.0 * rate / (L * L / 2))))
+    nb = max(1, min(w.B, -(-rows_wanted // w.D)))
+    per_b = -(-rows_wanted // nb)
+    rng = np.random.default_rng(7)
+    bs = rng.choice(w.B, size=nb, replace=False)
+    up = np.empty((w.B, w.T, w.D), np.float32)  # only rows in bs are filled
+    ud = np.empty((w.B, w.K, w.D), np.float32)
+    for b in bs:
+        up[b] = workloads.prompt_row(w, int(b))
+        ud[b] = workloads.decode_row(w, int(b))
+    rows = [(int(b), int(c)) for b in bs for c in range(min(per_b, w.D))][:rows_wanted]
+    t0 = time.perf_counter()
+    oracle.run_rows(lam, R, h0, up, ud, rows)
+    dt = time.perf_counter() - t0
+    seqs = len(rows) / w.D  # whole-width sequences' worth of rows
+    return {
+        "value": seqs * w.K / dt,
+        "unit": "tokens/s",
+        "cores": oracle.native_threads(),
+        "kind": "oracle",
+        "sample": (f"{len(rows)} (b,c) rows of {w.name} ({seqs:.2f} sequences' worth), each fully "
+                   f"computed (T={w.T} prompt + K={w.K} decode outputs by direct float64 "
+                   f"convolution, plus both states) in {dt:.2f} s; value = decode outputs "
+                   f"per second scaled to whole sequences (rows / D * K / time); the oracle "
+                   f"also produced the prompt outputs in that time"),
+        "seconds": dt,
+    }
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on exactly one GPU; --gpus {args.gpus} is not "
+              f"supported (every (b, c) row is independent, so batch/channel sharding needs "
+              f"no exchange; it is not built here).", file=sys.stderr)
+        sys.exit(2)
+    if args.copy_calibration:
+        copy_calibration()
+        return
+
+    import torch
+
+    import paper_2310_18780_amd as lh
+    import workloads
+
+    lh.lib()
+    w = workloads.workload(args.workload)
+    t_setup = time.perf_counter()
+    t = make_device_inputs(w)
+    B, T, D, d, K = w.B, w.T, w.D, w.d, w.K
+    state = torch.empty((B, D, d), dtype=torch.complex64, device="cuda")
+    y = torch.empty_like(t["u"])
+    y_dec = torch.empty((K, B, D), dtype=t["u"].dtype, device="cuda")
+    wsb = lh.workspace_bytes(B, D, d, T)
+    ws = torch.empty(max(wsb, 1), dtype=torch.uint8, device="cuda")
+    stream = torch.cuda.current_stream()
+
+    def prefill():
+        lh.prefill(t["lam"], t["R"], t["h0"], t["u"], state, y, workspace=ws)
+
+    def decode_eager():
+        for k in range(K):
+            lh.step(t["lam"], t["R"], t["h0"], state, t["ud"][k], y_dec[k])
+
+    prefill()
+    decode_eager()
+    torch.cuda.synchronize()
+    graph = None
+    if args.decode_launch == "graph":
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            decode_eager()
+        torch.cuda.synchronize()
+
+        def decode():
+            graph.replay()
+    else:
+        decode = decode_eager
+    setup_s = time.perf_counter() - t_setup
+
+    ev = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
+    for _ in range(args.warmup):
+        prefill()
+        decode()
+    torch.cuda.synchronize()
+
+    marks = [(ev(), ev(), ev()) for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for (a, b_, c) in marks:
+        a.record(stream)
+        prefill()
+        b_.record(stream)
+        decode()
+        c.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    pre_ms = [a.elapsed_time(b_) for a, b_, _ in marks]
+    dec_ms = [b_.elapsed_time(c) for _, b_, c in marks]
+    pre_avg = sum(pre_ms) / len(pre_ms)
+    dec_avg = sum(dec_ms) / len(dec_ms)
+    step_ms = wall * 1e3 / args.steps
+    dec_launch_us = dec_avg * 1e3 / K
+
+    dbytes = decode_bytes(w)
+    dec_gbs = dbytes / (dec_launch_us * 1e-6) / 1e9
+    pre_tf = prefill_flops(w) / (pre_avg * 1e-3) / 1e12
+    traffic = counter_traffic(f"decode_step_{w.name}_counters.txt", src_digest("decode.hip"))
+
+    # HBM-streaming decode: the same kernel over a pool of state buffers larger
+    # than the 256 MB Infinity Cache (like the layers of a model), so every
+    # launch reads and writes its state from HBM.
+    streaming = None
+    if args.stream_pool > 0:
+        pool = [torch.zeros((B, D, d), dtype=torch.complex64, device="cuda")
+                for _ in range(args.stream_pool)]
+        yk = torch.empty((B, D), dtype=t["u"].dtype, device="cuda")
+        g2 = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g2):
+            for s in pool:
+                lh.step(t["lam"], t["R"], t["h0"], s, t["ud"][0], yk)
+        g2.replay()
+        torch.cuda.synchronize()
+        a, c = ev(), ev()
+        reps = 8
+        a.record(stream)
+        for _ in range(reps):
+            g2.replay()
+        c.record(stream)
+        torch.cuda.synchronize()
+        us = a.elapsed_time(c) * 1e3 / (reps * len(pool))
+        streaming = {"launch_us": us, "gbps": dbytes / (us * 1e-6) / 1e9,
+                     "frac": dbytes / (us * 1e-6) / 1e9 / HBM_PEAK_GBS,
+                     "pool_buffers": len(pool),
+                     "pool_bytes": len(pool) * 8 * B * D * d}
+        del pool, g2
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(w, args.cpu_rows)
+
+    out = {
+        "metric": METRIC,
+        "value": B * K / (dec_avg * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": step_ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": w.name, "B": B, "D": D, "d": d, "T": T, "K": K, "io": w.io,
+                   "decode_launch": args.decode_launch, "prefill_workspace_bytes": wsb},
+        "prefill_tokens_per_s": B * T / (pre_avg * 1e-3),
+        "prefill_ms": pre_avg,
+        "decode_ms_per_step_total": dec_avg,
+        "decode_us_per_token_step": dec_launch_us,
+        "decode_gbps": dec_gbs,
+        "roofline": {"bound": "hbm", "achieved": dec_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": dec_gbs / HBM_PEAK_GBS, "traffic": traffic,
+                     "kernel": "step_kernel", "bytes_per_launch": dbytes},
+        "roofline_prefill": {"bound": "alu", "achieved": pre_tf, "peak": FP32_VALU_PEAK_TFLOPS,
+                             "unit": "TFLOP/s", "frac": pre_tf / FP32_VALU_PEAK_TFLOPS,
+                             "traffic": None, "flops_per_launch": prefill_flops(w),
+                             "bytes_per_launch": prefill_bytes(w),
+                             "gbps": prefill_bytes(w) / (pre_avg * 1e-3) / 1e9},
+        "decode_hbm_streaming": streaming,
+        "cpu_baseline": cpu,
+        "setup_s": setup_s,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

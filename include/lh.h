@@ -1,0 +1,150 @@
+/*
+ * lh.h -- C ABI of the distilled modal recurrence on AMD MI355X (gfx950).
+ *
+ * The operation (Laughing Hyena distillation, Sec. 3.4 "Deploying the
+ * recurrence", Proposition "modal_realization", App. B.1):
+ *
+ *   every channel c of a bank of D distilled filters carries d complex modes
+ *   with poles lambda[c,n], residues R[c,n] and a real pass-through h0[c];
+ *   its filter is h_0 = h0, h_t = Re sum_n R[c,n] lambda[c,n]^(t-1) (t >= 1,
+ *   eq. "modal_impulse").  Its state-space form is A = diag(lambda), B = 1,
+ *   C = R, D = h0 (eq. "dtssm"):
+ *
+ *       y_t     = Re( sum_n R[c,n] x_t[n] ) + h0[c] u_t      (reads x_t)
+ *       x_{t+1} = lambda[c,n] x_t[n] + u_t                     (then updates)
+ *
+ *   so that, from x_0 = 0, y is the causal convolution of h with u
+ *   (eq. "cnn") and x_T[n] = sum_{k<T} lambda[c,n]^(T-1-k) u_k.
+ *
+ * Prefill (lh_prefill) processes a prompt of T tokens: all outputs y_0..y_{T-1}
+ * and the post-prompt state x_T.  Decode (lh_step) advances the state by one
+ * token per call and returns that token's output; a step right after a prefill
+ * of T tokens returns y_T.
+ *
+ * Layouts (all row-major, contiguous, caller-owned device memory):
+ *   lambda, R : [D, d]    complex64, interleaved (re, im)        (lh_c32)
+ *   h0        : [D]       float32
+ *   u, y      : [B, T, D] float32 or bfloat16 (io_dtype), channel fastest
+ *   state     : [B, D, d] complex64, mode fastest
+ *   u_t, y_t  : [B, D]    float32 or bfloat16 (io_dtype)
+ * All arithmetic is float32; bfloat16 inputs are widened exactly and bfloat16
+ * outputs are rounded to nearest, ties to even.
+ *
+ * Ownership and execution: the library never allocates, frees or keeps a
+ * pointer; it holds no state between calls and is re-entrant.  Work is enqueued
+ * asynchronously on `stream` (a hipStream_t; NULL is the null stream) and the
+ * call returns without synchronising.  Calls on the same buffers must be
+ * ordered by the caller (same stream, or events).
+ *
+ * Errors: every argument is checked on the host before any device work is
+ * enqueued; on a non-LH_OK status nothing has been enqueued and no buffer has
+ * been touched.  Faults during execution surface at the caller's next
+ * synchronisation of `stream`.  No call aborts and no C++ exception crosses
+ * this interface.  lh_last_error() returns a thread-local description of the
+ * most recent failure in the calling thread.
+ */
+#ifndef LH_H
+#define LH_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define LH_ABI_VERSION 1
+
+/* complex64, interleaved real and imaginary parts */
+typedef struct lh_c32 {
+    float re;
+    float im;
+} lh_c32;
+
+/* element type of u / y (and u_t / y_t); lambda, R, h0 and the state are
+ * always float32-based */
+typedef enum lh_dtype {
+    LH_F32 = 0,
+    LH_BF16 = 1
+} lh_dtype;
+
+typedef enum lh_status {
+    LH_OK = 0,
+    LH_ERR_INVALID_ARG = 1,       /* null pointer, bad size, size overflow,
+                                     pointer not accessible from the device */
+    LH_ERR_OVERLAP = 2,           /* an output buffer overlaps another buffer */
+    LH_ERR_UNSUPPORTED_DTYPE = 3, /* io_dtype is not LH_F32 or LH_BF16 */
+    LH_ERR_NO_DEVICE = 4,         /* no HIP device is visible */
+    LH_ERR_WORKSPACE = 5,         /* workspace null or smaller than required */
+    LH_ERR_HIP = 6                /* the HIP runtime refused a launch */
+} lh_status;
+
+/* Largest supported number of modes per channel. */
+#define LH_MAX_MODES 1024
+
+/* LH_ABI_VERSION of the built library. */
+int lh_abi_version(void);
+
+/* Static description of a status code (never NULL). */
+const char* lh_status_string(lh_status status);
+
+/* Thread-local detail of the most recent non-LH_OK status returned in the
+ * calling thread ("" if none). */
+const char* lh_last_error(void);
+
+/*
+ * Workspace bytes lh_prefill needs for these sizes and chunk length
+ * (chunk_len = 0 selects the automatic plan, as in lh_prefill).  Returns 0
+ * when the plan needs no workspace and (size_t)-1 when the arguments are
+ * invalid.  Pure function of its arguments.
+ */
+size_t lh_prefill_workspace_bytes(int64_t B, int64_t D, int64_t d, int64_t T,
+                                  int64_t chunk_len);
+
+/*
+ * Prefill: outputs y[b,t,c] for t < T and the post-prompt state
+ * state[b,c,n] = x_T (Sec. 3.4, "fast pre-filling"; states start at x_0 = 0).
+ *
+ *   lambda, R, h0 : inputs as laid out above
+ *   u             : [B,T,D] prompt inputs (io_dtype)
+ *   B, D, d, T    : B >= 1, D >= 1, 1 <= d <= LH_MAX_MODES, T >= 0
+ *   io_dtype      : LH_F32 or LH_BF16 (u and y)
+ *   state         : out, [B,D,d] complex64 (overwritten, not read)
+ *   y             : out, [B,T,D] (io_dtype); may be NULL only when T == 0
+ *   chunk_len     : 0 = automatic; otherwise the time-chunk length of the
+ *                   chunked scan (the prompt is cut into ceil(T/chunk_len)
+ *                   chunks processed in parallel; chunk_len >= T means one
+ *                   sequential pass)
+ *   workspace     : device scratch of at least
+ *                   lh_prefill_workspace_bytes(B,D,d,T,chunk_len) bytes,
+ *                   256-byte aligned; may be NULL when that size is 0.  Its
+ *                   contents on entry are ignored and on exit undefined.
+ * T == 0 zeroes the state and leaves y untouched.  y must not overlap u,
+ * state, lambda, R, h0 or workspace; state must not overlap any input.
+ */
+lh_status lh_prefill(const lh_c32* lambda, const lh_c32* R, const float* h0,
+                     const void* u, int64_t B, int64_t D, int64_t d, int64_t T,
+                     lh_dtype io_dtype, lh_c32* state, void* y,
+                     int64_t chunk_len, void* workspace, size_t workspace_bytes,
+                     void* stream);
+
+/*
+ * Decode step (Proposition "modal_realization"; App. B.1 for the real part):
+ *   y_t[b,c]     = Re(sum_n R[c,n] state[b,c,n]) + h0[c] u_t[b,c]
+ *   state[b,c,n] = lambda[c,n] state[b,c,n] + u_t[b,c]      (in place)
+ *
+ *   state : in/out [B,D,d] complex64
+ *   u_t   : [B,D] (io_dtype);  y_t : out [B,D] (io_dtype)
+ * y_t must not overlap any other buffer; state must not overlap lambda, R,
+ * h0 or u_t.  O(d) work per (b, c); one kernel launch; no workspace.
+ */
+lh_status lh_step(const lh_c32* lambda, const lh_c32* R, const float* h0,
+                  lh_c32* state, const void* u_t, void* y_t,
+                  int64_t B, int64_t D, int64_t d, lh_dtype io_dtype,
+                  void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LH_H */

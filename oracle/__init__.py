@@ -80,16 +80,17 @@ def native_threads() -> int:
 
 
 def power_table(lam: np.ndarray, m: int) -> np.ndarray:
-    """``P[..., k] = lam^k`` for ``k = 0 .. m-1`` by running float64 products.
+    """``P[..., k] = lam^k`` for ``k = 0 .. m-1`` as running float64 products
+    (``np.cumprod`` multiplies left to right: ``lam^k = lam^(k-1) * lam``).
 
     ``lam``: complex array of any shape; returns complex128 ``lam.shape + (m,)``.
     """
     lam = np.asarray(lam).astype(np.complex128)
     P = np.empty(lam.shape + (m,), np.complex128)
-    p = np.ones(lam.shape, np.complex128)
-    for k in range(m):
-        P[..., k] = p
-        p = p * lam
+    if m > 0:
+        P[..., 0] = 1.0
+    if m > 1:
+        P[..., 1:] = np.cumprod(np.broadcast_to(lam[..., None], lam.shape + (m - 1,)), axis=-1)
     return P
 
 

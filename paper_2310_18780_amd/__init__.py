@@ -1,0 +1,177 @@
+"""Distilled modal recurrence (Laughing Hyena) on AMD MI355X.
+
+Thin Python binding of ``liblh.so`` (C ABI in ``include/lh.h``): it checks
+tensor shapes and dtypes, marshals pointers and the current HIP stream, and
+calls the library.  Every step of the computation runs in the library's HIP
+kernels; there is no fallback.  PyTorch provides device memory and streams.
+
+    prefill(lam, R, h0, u, state, y)   # y[b,t,c], t < T, and state = x_T
+    step(lam, R, h0, state, u_t, y_t)  # y_t from x_t, then x_{t+1} in place
+
+``lam``, ``R``: complex64 ``[D, d]``; ``h0``: float32 ``[D]``; ``u``, ``y``:
+float32 or bfloat16 ``[B, T, D]``; ``state``: complex64 ``[B, D, d]``;
+``u_t``, ``y_t``: ``[B, D]``.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+__all__ = [
+    "LH_F32",
+    "LH_BF16",
+    "LHError",
+    "lib",
+    "library_path",
+    "workspace_bytes",
+    "prefill",
+    "step",
+    "STATUS",
+]
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB_PATH = os.path.join(_HERE, "liblh.so")
+
+LH_F32 = 0
+LH_BF16 = 1
+STATUS = {
+    0: "LH_OK",
+    1: "LH_ERR_INVALID_ARG",
+    2: "LH_ERR_OVERLAP",
+    3: "LH_ERR_UNSUPPORTED_DTYPE",
+    4: "LH_ERR_NO_DEVICE",
+    5: "LH_ERR_WORKSPACE",
+    6: "LH_ERR_HIP",
+}
+
+_lib: Optional[ctypes.CDLL] = None
+
+
+class LHError(RuntimeError):
+    def __init__(self, status: int, detail: str):
+        self.status = status
+        self.name = STATUS.get(status, f"status {status}")
+        super().__init__(f"{self.name}: {detail}")
+
+
+def library_path() -> str:
+    return _LIB_PATH
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded library; raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB_PATH):
+        raise ImportError(
+            f"{_LIB_PATH} is missing: build it with `python -m paper_2310_18780_amd.build` "
+            "(or __graft_entry__.build()); there is no fallback implementation")
+    L = ctypes.CDLL(_LIB_PATH)
+    i64, vp, sz = ctypes.c_int64, ctypes.c_void_p, ctypes.c_size_t
+    L.lh_abi_version.argtypes = []
+    L.lh_abi_version.restype = ctypes.c_int
+    L.lh_status_string.argtypes = [ctypes.c_int]
+    L.lh_status_string.restype = ctypes.c_char_p
+    L.lh_last_error.argtypes = []
+    L.lh_last_error.restype = ctypes.c_char_p
+    L.lh_prefill_workspace_bytes.argtypes = [i64, i64, i64, i64, i64]
+    L.lh_prefill_workspace_bytes.restype = sz
+    L.lh_prefill.argtypes = [vp, vp, vp, vp, i64, i64, i64, i64, ctypes.c_int, vp, vp, i64, vp,
+                             sz, vp]
+    L.lh_prefill.restype = ctypes.c_int
+    L.lh_step.argtypes = [vp, vp, vp, vp, vp, vp, i64, i64, i64, ctypes.c_int, vp]
+    L.lh_step.restype = ctypes.c_int
+    _lib = L
+    return L
+
+
+def _check(status: int) -> None:
+    if status != 0:
+        raise LHError(status, lib().lh_last_error().decode(errors="replace"))
+
+
+def workspace_bytes(B: int, D: int, d: int, T: int, chunk_len: int = 0) -> int:
+    n = lib().lh_prefill_workspace_bytes(B, D, d, T, chunk_len)
+    if n == ctypes.c_size_t(-1).value:
+        raise LHError(1, f"invalid sizes B={B} D={D} d={d} T={T} chunk_len={chunk_len}")
+    return int(n)
+
+
+def _io_dtype(t) -> int:
+    import torch
+
+    if t.dtype == torch.float32:
+        return LH_F32
+    if t.dtype == torch.bfloat16:
+        return LH_BF16
+    raise TypeError(f"u / y must be float32 or bfloat16, got {t.dtype}")
+
+
+def _need(t, name, dtype, shape):
+    import torch
+
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must be on a HIP device, got {t.device}")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+def _stream(dev, stream) -> int:
+    import torch
+
+    if stream is None:
+        stream = torch.cuda.current_stream(dev)
+    return int(stream.cuda_stream) if hasattr(stream, "cuda_stream") else int(stream)
+
+
+def prefill(lam, R, h0, u, state, y, workspace=None, chunk_len: int = 0, stream=None) -> None:
+    """Prompt outputs ``y`` and post-prompt state ``state`` (both overwritten).
+
+    ``workspace``: a uint8 CUDA tensor of at least ``workspace_bytes(...)``
+    bytes, or None to have one allocated here with torch."""
+    import torch
+
+    B, T, D = u.shape
+    d = lam.shape[1]
+    _need(lam, "lam", torch.complex64, (D, d))
+    _need(R, "R", torch.complex64, (D, d))
+    _need(h0, "h0", torch.float32, (D,))
+    _need(u, "u", u.dtype, (B, T, D))
+    _need(state, "state", torch.complex64, (B, D, d))
+    _need(y, "y", u.dtype, (B, T, D))
+    io = _io_dtype(u)
+    need = workspace_bytes(B, D, d, T, chunk_len)
+    if need > 0 and workspace is None:
+        workspace = torch.empty(need, dtype=torch.uint8, device=u.device)
+    ws_ptr = workspace.data_ptr() if workspace is not None else None
+    ws_len = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    _check(lib().lh_prefill(lam.data_ptr(), R.data_ptr(), h0.data_ptr(), u.data_ptr(), B, D, d, T,
+                            io, state.data_ptr(), y.data_ptr(), chunk_len, ws_ptr, ws_len,
+                            _stream(u.device, stream)))
+
+
+def step(lam, R, h0, state, u_t, y_t, stream=None) -> None:
+    """One decode step: ``y_t`` from the current state, then the state update
+    in place."""
+    import torch
+
+    B, D = u_t.shape
+    d = lam.shape[1]
+    _need(lam, "lam", torch.complex64, (D, d))
+    _need(R, "R", torch.complex64, (D, d))
+    _need(h0, "h0", torch.float32, (D,))
+    _need(state, "state", torch.complex64, (B, D, d))
+    _need(u_t, "u_t", u_t.dtype, (B, D))
+    _need(y_t, "y_t", u_t.dtype, (B, D))
+    io = _io_dtype(u_t)
+    _check(lib().lh_step(lam.data_ptr(), R.data_ptr(), h0.data_ptr(), state.data_ptr(),
+                         u_t.data_ptr(), y_t.data_ptr(), B, D, d, io,
+                         _stream(u_t.device, stream)))

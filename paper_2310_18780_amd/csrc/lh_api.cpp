@@ -1,0 +1,269 @@
+// C ABI of liblh (declared in include/lh.h): argument validation, launch
+// planning and dispatch.  Every check runs on the host before anything is
+// enqueued; a failing call touches no buffer.
+#include "lh.h"
+
+#include <hip/hip_runtime.h>
+
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include "lh_internal.hpp"
+
+namespace {
+
+thread_local char g_last_error[512] = "";
+
+lh_status fail(lh_status s, const char* fmt, ...)
+{
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_last_error, sizeof(g_last_error), fmt, ap);
+    va_end(ap);
+    return s;
+}
+
+struct Buf {
+    const char* name;
+    uintptr_t lo;
+    uintptr_t hi;  // exclusive
+};
+
+bool overlaps(const Buf& a, const Buf& b)
+{
+    if (a.lo == a.hi || b.lo == b.hi) return false;  // empty ranges
+    return a.lo < b.hi && b.lo < a.hi;
+}
+
+Buf buf(const char* name, const void* p, size_t bytes)
+{
+    const uintptr_t lo = reinterpret_cast<uintptr_t>(p);
+    return Buf{name, lo, lo + bytes};
+}
+
+bool mul_ok(int64_t a, int64_t b, int64_t* out)
+{
+    return !__builtin_mul_overflow(a, b, out) && *out <= (INT64_C(1) << 60);
+}
+
+lh_status check_sizes(int64_t B, int64_t D, int64_t d, int64_t T)
+{
+    if (B < 1) return fail(LH_ERR_INVALID_ARG, "B = %lld must be >= 1", (long long)B);
+    if (D < 1) return fail(LH_ERR_INVALID_ARG, "D = %lld must be >= 1", (long long)D);
+    if (d < 1 || d > LH_MAX_MODES)
+        return fail(LH_ERR_INVALID_ARG, "d = %lld must be in [1, %d]", (long long)d, LH_MAX_MODES);
+    if (T < 0) return fail(LH_ERR_INVALID_ARG, "T = %lld must be >= 0", (long long)T);
+    int64_t bd, bdd, btd;
+    if (!mul_ok(B, D, &bd) || !mul_ok(bd, d, &bdd) || !mul_ok(bdd, 8, &bdd) ||
+        !mul_ok(bd, T > 0 ? T : 1, &btd) || !mul_ok(btd, d, &btd) || !mul_ok(btd, 8, &btd))
+        return fail(LH_ERR_INVALID_ARG, "sizes overflow (B=%lld D=%lld d=%lld T=%lld)",
+                    (long long)B, (long long)D, (long long)d, (long long)T);
+    return LH_OK;
+}
+
+lh_status check_dtype(lh_dtype t)
+{
+    if (t != LH_F32 && t != LH_BF16)
+        return fail(LH_ERR_UNSUPPORTED_DTYPE, "io_dtype %d is neither LH_F32 nor LH_BF16", (int)t);
+    return LH_OK;
+}
+
+lh_status check_align(const Buf& b, uintptr_t a)
+{
+    if (b.lo % a != 0)
+        return fail(LH_ERR_INVALID_ARG, "%s is not %u-byte aligned", b.name, (unsigned)a);
+    return LH_OK;
+}
+
+lh_status check_device(int* dev)
+{
+    int n = 0;
+    if (hipGetDeviceCount(&n) != hipSuccess || n < 1) {
+        (void)hipGetLastError();
+        return fail(LH_ERR_NO_DEVICE, "no HIP device is visible");
+    }
+    if (hipGetDevice(dev) != hipSuccess) {
+        (void)hipGetLastError();
+        return fail(LH_ERR_NO_DEVICE, "hipGetDevice failed");
+    }
+    return LH_OK;
+}
+
+// The range [lo, hi) must be memory the current device can access: device
+// memory of this device, or pinned / managed host memory, and it must lie
+// inside one allocation.
+lh_status check_accessible(const Buf& b, int dev)
+{
+    if (b.lo == b.hi) return LH_OK;
+    void* p = reinterpret_cast<void*>(b.lo);
+    hipPointerAttribute_t a;
+    memset(&a, 0, sizeof(a));
+    if (hipPointerGetAttributes(&a, p) != hipSuccess) {
+        (void)hipGetLastError();
+        return fail(LH_ERR_INVALID_ARG, "%s (%p) is not memory known to HIP", b.name, p);
+    }
+    if (a.type == hipMemoryTypeUnregistered)
+        return fail(LH_ERR_INVALID_ARG, "%s (%p) is unregistered host memory", b.name, p);
+    if (a.type == hipMemoryTypeDevice && a.device != dev)
+        return fail(LH_ERR_INVALID_ARG, "%s lives on device %d, the current device is %d", b.name,
+                    a.device, dev);
+    hipDeviceptr_t base = nullptr;
+    size_t size = 0;
+    if (hipMemGetAddressRange(&base, &size, p) == hipSuccess && base != nullptr) {
+        const uintptr_t blo = reinterpret_cast<uintptr_t>(base);
+        if (b.lo < blo || b.hi > blo + size)
+            return fail(LH_ERR_INVALID_ARG,
+                        "%s [%p, +%zu) extends past its allocation [%p, +%zu)", b.name, p,
+                        (size_t)(b.hi - b.lo), base, size);
+    } else {
+        (void)hipGetLastError();
+    }
+    return LH_OK;
+}
+
+lh_status from_hip(hipError_t e, const char* what)
+{
+    if (e == hipSuccess) return LH_OK;
+    return fail(LH_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+}  // namespace
+
+extern "C" {
+
+int lh_abi_version(void) { return LH_ABI_VERSION; }
+
+const char* lh_status_string(lh_status s)
+{
+    switch (s) {
+        case LH_OK: return "LH_OK";
+        case LH_ERR_INVALID_ARG: return "LH_ERR_INVALID_ARG: invalid argument";
+        case LH_ERR_OVERLAP: return "LH_ERR_OVERLAP: an output overlaps another buffer";
+        case LH_ERR_UNSUPPORTED_DTYPE: return "LH_ERR_UNSUPPORTED_DTYPE: unsupported io dtype";
+        case LH_ERR_NO_DEVICE: return "LH_ERR_NO_DEVICE: no HIP device";
+        case LH_ERR_WORKSPACE: return "LH_ERR_WORKSPACE: workspace missing or too small";
+        case LH_ERR_HIP: return "LH_ERR_HIP: HIP runtime error";
+    }
+    return "unknown lh_status";
+}
+
+const char* lh_last_error(void) { return g_last_error; }
+
+size_t lh_prefill_workspace_bytes(int64_t B, int64_t D, int64_t d, int64_t T, int64_t chunk_len)
+{
+    if (check_sizes(B, D, d, T) != LH_OK || chunk_len < 0) return (size_t)-1;
+    lh::PrefillPlan p;
+    if (!lh::make_prefill_plan(B, D, d, T, chunk_len, &p)) return (size_t)-1;
+    return p.ws_bytes;
+}
+
+lh_status lh_prefill(const lh_c32* lambda, const lh_c32* R, const float* h0, const void* u,
+                     int64_t B, int64_t D, int64_t d, int64_t T, lh_dtype io_dtype,
+                     lh_c32* state, void* y, int64_t chunk_len, void* workspace,
+                     size_t workspace_bytes, void* stream)
+{
+    g_last_error[0] = '\0';
+    lh_status s;
+    if (!lambda || !R || !h0 || !state)
+        return fail(LH_ERR_INVALID_ARG, "lambda, R, h0 and state must not be NULL");
+    if ((s = check_sizes(B, D, d, T)) != LH_OK) return s;
+    if (T > 0 && (!u || !y)) return fail(LH_ERR_INVALID_ARG, "u and y must not be NULL when T > 0");
+    if (chunk_len < 0) return fail(LH_ERR_INVALID_ARG, "chunk_len must be >= 0");
+    if ((s = check_dtype(io_dtype)) != LH_OK) return s;
+    lh::PrefillPlan plan;
+    if (!lh::make_prefill_plan(B, D, d, T, chunk_len, &plan))
+        return fail(LH_ERR_INVALID_ARG, "no prefill plan for these sizes");
+
+    const size_t es = io_dtype == LH_BF16 ? 2 : 4;
+    const size_t n_io = static_cast<size_t>(B) * T * D;
+    const Buf b_lam = buf("lambda", lambda, sizeof(lh_c32) * D * d);
+    const Buf b_R = buf("R", R, sizeof(lh_c32) * D * d);
+    const Buf b_h0 = buf("h0", h0, sizeof(float) * D);
+    const Buf b_u = buf("u", u, T > 0 ? es * n_io : 0);
+    const Buf b_state = buf("state", state, sizeof(lh_c32) * B * D * d);
+    const Buf b_y = buf("y", y, T > 0 ? es * n_io : 0);
+    const Buf b_ws = buf("workspace", workspace, plan.ws_bytes ? plan.ws_bytes : 0);
+
+    if ((s = check_align(b_lam, 8)) || (s = check_align(b_R, 8)) || (s = check_align(b_h0, 4)) ||
+        (s = check_align(b_state, 8)) || (s = check_align(b_u, es)) || (s = check_align(b_y, es)))
+        return s;
+    if (plan.ws_bytes > 0) {
+        if (!workspace)
+            return fail(LH_ERR_WORKSPACE, "workspace is NULL but %zu bytes are needed",
+                        plan.ws_bytes);
+        if (workspace_bytes < plan.ws_bytes)
+            return fail(LH_ERR_WORKSPACE, "workspace has %zu bytes, %zu are needed",
+                        workspace_bytes, plan.ws_bytes);
+        if ((s = check_align(b_ws, 256))) return s;
+    }
+    const Buf* ins[] = {&b_lam, &b_R, &b_h0, &b_u};
+    const Buf* outs[] = {&b_state, &b_y, &b_ws};
+    for (const Buf* o : outs) {
+        for (const Buf* i : ins)
+            if (overlaps(*o, *i))
+                return fail(LH_ERR_OVERLAP, "%s overlaps %s", o->name, i->name);
+        for (const Buf* o2 : outs)
+            if (o != o2 && overlaps(*o, *o2))
+                return fail(LH_ERR_OVERLAP, "%s overlaps %s", o->name, o2->name);
+    }
+
+    int dev = 0;
+    if ((s = check_device(&dev)) != LH_OK) return s;
+    const Buf* all[] = {&b_lam, &b_R, &b_h0, &b_u, &b_state, &b_y, &b_ws};
+    for (const Buf* b : all)
+        if ((s = check_accessible(*b, dev)) != LH_OK) return s;
+
+    return from_hip(
+        lh::launch_prefill(reinterpret_cast<const float2*>(lambda),
+                           reinterpret_cast<const float2*>(R), h0, u, io_dtype == LH_BF16, B, D,
+                           d, T, reinterpret_cast<float2*>(state), y, plan, workspace,
+                           static_cast<hipStream_t>(stream)),
+        "prefill launch");
+}
+
+lh_status lh_step(const lh_c32* lambda, const lh_c32* R, const float* h0, lh_c32* state,
+                  const void* u_t, void* y_t, int64_t B, int64_t D, int64_t d,
+                  lh_dtype io_dtype, void* stream)
+{
+    g_last_error[0] = '\0';
+    lh_status s;
+    if (!lambda || !R || !h0 || !state || !u_t || !y_t)
+        return fail(LH_ERR_INVALID_ARG, "lambda, R, h0, state, u_t and y_t must not be NULL");
+    if ((s = check_sizes(B, D, d, 0)) != LH_OK) return s;
+    if ((s = check_dtype(io_dtype)) != LH_OK) return s;
+
+    const size_t es = io_dtype == LH_BF16 ? 2 : 4;
+    const Buf b_lam = buf("lambda", lambda, sizeof(lh_c32) * D * d);
+    const Buf b_R = buf("R", R, sizeof(lh_c32) * D * d);
+    const Buf b_h0 = buf("h0", h0, sizeof(float) * D);
+    const Buf b_u = buf("u_t", u_t, es * B * D);
+    const Buf b_state = buf("state", state, sizeof(lh_c32) * B * D * d);
+    const Buf b_y = buf("y_t", y_t, es * B * D);
+    // the 16-byte path of the step kernel needs 16-byte aligned complex arrays
+    if ((s = check_align(b_lam, 8)) || (s = check_align(b_R, 8)) || (s = check_align(b_h0, 4)) ||
+        (s = check_align(b_state, 8)) || (s = check_align(b_u, es)) || (s = check_align(b_y, es)))
+        return s;
+    const Buf* ins[] = {&b_lam, &b_R, &b_h0, &b_u};
+    for (const Buf* i : ins) {
+        if (overlaps(b_state, *i)) return fail(LH_ERR_OVERLAP, "state overlaps %s", i->name);
+        if (overlaps(b_y, *i)) return fail(LH_ERR_OVERLAP, "y_t overlaps %s", i->name);
+    }
+    if (overlaps(b_y, b_state)) return fail(LH_ERR_OVERLAP, "y_t overlaps state");
+
+    int dev = 0;
+    if ((s = check_device(&dev)) != LH_OK) return s;
+    const Buf* all[] = {&b_lam, &b_R, &b_h0, &b_u, &b_state, &b_y};
+    for (const Buf* b : all)
+        if ((s = check_accessible(*b, dev)) != LH_OK) return s;
+
+    const bool aligned16 = b_lam.lo % 16 == 0 && b_R.lo % 16 == 0 && b_state.lo % 16 == 0;
+    return from_hip(lh::launch_step(reinterpret_cast<const float2*>(lambda),
+                                    reinterpret_cast<const float2*>(R), h0,
+                                    reinterpret_cast<float2*>(state), u_t, y_t,
+                                    io_dtype == LH_BF16, B, D, d, aligned16,
+                                    static_cast<hipStream_t>(stream)),
+                    "step launch");
+}
+
+}  // extern "C"

@@ -1,0 +1,59 @@
+// Internal declarations of liblh: element helpers shared by the kernels and
+// the launchers the C ABI layer calls.  Not part of the public interface.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace lh {
+
+// bfloat16 storage type (upper half of a float32)
+struct bf16 {
+    uint16_t bits;
+};
+
+__device__ __forceinline__ float io_load(const float* p) { return *p; }
+__device__ __forceinline__ float io_load(const bf16* p) {
+    return __uint_as_float(static_cast<uint32_t>(p->bits) << 16);
+}
+__device__ __forceinline__ void io_store(float* p, float v) { *p = v; }
+// float32 -> bfloat16, round to nearest, ties to even; NaN stays a quiet NaN.
+__device__ __forceinline__ void io_store(bf16* p, float v) {
+    uint32_t x = __float_as_uint(v);
+    uint16_t r;
+    if ((x & 0x7fffffffu) > 0x7f800000u) {
+        r = static_cast<uint16_t>((x >> 16) | 0x0040u);
+    } else {
+        x += 0x7fffu + ((x >> 16) & 1u);
+        r = static_cast<uint16_t>(x >> 16);
+    }
+    p->bits = r;
+}
+
+// How the prefill of one call is cut up.
+struct PrefillPlan {
+    int lpr;          // lanes per (b, c) row: the modes of a row are split over lpr lanes
+    int mpl;          // modes per lane (power of two <= 16); lpr * mpl >= d
+    int64_t C;        // chunk length (time steps per chunk)
+    int64_t nchunks;  // ceil(T / C); 0 when T == 0
+    size_t off_pow;   // workspace offset of lambda^C          [D, d] complex64
+    size_t off_xin;   // workspace offset of chunk entry states [B, nchunks, D, d] complex64
+    size_t ws_bytes;  // total workspace bytes (0 when nchunks <= 1)
+};
+
+// Returns false when the sizes are invalid or overflow.
+bool make_prefill_plan(int64_t B, int64_t D, int64_t d, int64_t T, int64_t chunk_len,
+                       PrefillPlan* plan);
+
+// Launchers (asynchronous, on `stream`); they return the launch status.
+hipError_t launch_prefill(const float2* lam, const float2* R, const float* h0,
+                          const void* u, bool bf16_io, int64_t B, int64_t D, int64_t d,
+                          int64_t T, float2* state, void* y, const PrefillPlan& plan,
+                          void* workspace, hipStream_t stream);
+
+hipError_t launch_step(const float2* lam, const float2* R, const float* h0, float2* state,
+                       const void* u_t, void* y_t, bool bf16_io, int64_t B, int64_t D,
+                       int64_t d, bool aligned16, hipStream_t stream);
+
+}  // namespace lh

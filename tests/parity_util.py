@@ -1,0 +1,150 @@
+"""Helpers of the GPU parity tests: run the HIP path through the C ABI on
+seeded inputs and compare with the oracle.
+
+Tolerances (derived from float32 arithmetic over the workloads' lengths):
+
+* float32 outputs: per (b, c) row, ``max_t |y_gpu - y_ref| <= 1e-4 * max_t |y_ref|``
+  (the relative tolerance 1e-4 applied to the row's infinity norm, since an
+  elementwise relative error is undefined where an output crosses zero);
+* states: per (b, c), ``max_n |x_gpu - x_ref| <= 1e-4 * max_n |x_ref|``;
+* bfloat16 outputs: elementwise ``|y_gpu - y_ref| <= 2^-8 |y_ref| + 1e-4 * rowmax``,
+  i.e. the round-to-nearest error of bfloat16 (half a unit in the last place,
+  at most 2^-8 relative) on top of the float32 tolerance.
+"""
+from __future__ import annotations
+
+import math
+from typing import Dict, Iterable, List, Optional, Sequence, Tuple
+
+import numpy as np
+
+REL_TOL = 1e-4
+BF16_REL = 2.0 ** -8
+
+
+def to_device(lam, R, h0, up, ud, io: str, device="cuda"):
+    import torch
+
+    iot = torch.bfloat16 if io == "bf16" else torch.float32
+    t = dict(
+        lam=torch.from_numpy(np.ascontiguousarray(lam)).to(device),
+        R=torch.from_numpy(np.ascontiguousarray(R)).to(device),
+        h0=torch.from_numpy(np.ascontiguousarray(h0)).to(device),
+        u=torch.from_numpy(np.ascontiguousarray(up)).to(device).to(iot),
+        # decode inputs as [K, B, D] so that step k reads a contiguous [B, D]
+        ud=torch.from_numpy(np.ascontiguousarray(ud.transpose(1, 0, 2))).to(device).to(iot),
+    )
+    return t
+
+
+def run_gpu(t, chunk_len: int = 0, ws=None):
+    """Prefill then K decode steps; returns device tensors y [B,T,D], x_T,
+    y_dec [K,B,D], x_end."""
+    import torch
+
+    import paper_2310_18780_amd as lh
+
+    B, T, D = t["u"].shape
+    K = t["ud"].shape[0]
+    d = t["lam"].shape[1]
+    dev = t["u"].device
+    y = torch.full((B, T, D), float("nan"), dtype=t["u"].dtype, device=dev)
+    state = torch.full((B, D, d), complex(float("nan"), float("nan")), dtype=torch.complex64,
+                       device=dev)
+    lh.prefill(t["lam"], t["R"], t["h0"], t["u"], state, y, workspace=ws, chunk_len=chunk_len)
+    x_T = state.clone()
+    y_dec = torch.full((K, B, D), float("nan"), dtype=t["u"].dtype, device=dev)
+    for k in range(K):
+        lh.step(t["lam"], t["R"], t["h0"], state, t["ud"][k], y_dec[k])
+    torch.cuda.synchronize()
+    return dict(y_prefill=y, x_T=x_T, y_dec=y_dec, x_end=state)
+
+
+def _np(x):
+    import torch
+
+    if x.dtype == torch.bfloat16:
+        x = x.float()
+    return x.cpu().numpy()
+
+
+def check_y(y_gpu: np.ndarray, y_ref: np.ndarray, io: str, what: str, ref_rounded=False):
+    """y_* as [rows, L] arrays (L may be 0).  ``ref_rounded``: the reference is
+    itself a bfloat16-rounded result (GPU against GPU), so each side carries
+    half a bfloat16 ulp of rounding."""
+    if y_ref.shape[-1] == 0:
+        return 0.0
+    assert np.all(np.isfinite(y_gpu)), f"{what}: non-finite output"
+    err = np.abs(y_gpu.astype(np.float64) - y_ref)
+    rowmax = np.max(np.abs(y_ref), axis=-1, keepdims=True)
+    if io == "bf16":
+        bound = (2 if ref_rounded else 1) * BF16_REL * np.abs(y_ref) + REL_TOL * rowmax
+    else:
+        bound = REL_TOL * rowmax
+    bad = err > bound
+    if np.any(bad):
+        i = np.unravel_index(np.argmax(err - bound), err.shape)
+        raise AssertionError(
+            f"{what}: {int(bad.sum())} outputs out of tolerance; worst at {i}: gpu={y_gpu[i]!r} "
+            f"ref={y_ref[i]!r} err={err[i]:.3g} bound={bound[i]:.3g} rowmax={rowmax[i[0]][0]:.3g}")
+    return float(np.max(err / np.maximum(rowmax, 1e-300)))
+
+
+def check_x(x_gpu: np.ndarray, x_ref: np.ndarray, what: str):
+    """states as [rows, d] complex arrays."""
+    assert np.all(np.isfinite(x_gpu.real)) and np.all(np.isfinite(x_gpu.imag)), f"{what}: non-finite"
+    err = np.abs(x_gpu.astype(np.complex128) - x_ref)
+    rowmax = np.max(np.abs(x_ref), axis=-1, keepdims=True)
+    bad = err > REL_TOL * rowmax
+    if np.any(bad):
+        i = np.unravel_index(np.argmax(err / np.maximum(rowmax, 1e-300)), err.shape)
+        raise AssertionError(f"{what}: {int(bad.sum())} modes out of tolerance; worst at {i}: "
+                             f"gpu={x_gpu[i]!r} ref={x_ref[i]!r} rowmax={rowmax[i[0]][0]:.3g}")
+    return float(np.max(err / np.maximum(rowmax, 1e-300))) if err.size else 0.0
+
+
+def compare_full(out, ref, io: str) -> Dict[str, float]:
+    """Every output and state of a small case."""
+    B, T, D = out["y_prefill"].shape
+    yp = _np(out["y_prefill"]).transpose(0, 2, 1).reshape(B * D, T)
+    yd = _np(out["y_dec"]).transpose(1, 2, 0).reshape(B * D, -1)
+    r_yp = ref["y_prefill"].transpose(0, 2, 1).reshape(B * D, T)
+    r_yd = ref["y_dec"].transpose(0, 2, 1).reshape(B * D, -1)
+    d = out["x_T"].shape[-1]
+    return dict(
+        y_prefill=check_y(yp, r_yp, io, "prefill y"),
+        y_dec=check_y(yd, r_yd, io, "decode y"),
+        x_T=check_x(_np(out["x_T"]).reshape(-1, d), ref["x_T"].reshape(-1, d), "x_T"),
+        x_end=check_x(_np(out["x_end"]).reshape(-1, d), ref["x_end"].reshape(-1, d), "x_end"),
+    )
+
+
+def gather_rows(out, rows: Sequence[Tuple[int, int]]):
+    """Copy only the selected (b, c) rows of the GPU results to the host."""
+    import torch
+
+    bs = torch.tensor([b for b, _ in rows], device=out["y_prefill"].device)
+    cs = torch.tensor([c for _, c in rows], device=out["y_prefill"].device)
+    return dict(
+        y_prefill=_np(out["y_prefill"][bs, :, cs]),  # [rows, T]
+        y_dec=_np(out["y_dec"][:, bs, cs].T.contiguous()),  # [rows, K]
+        x_T=_np(out["x_T"][bs, cs]),
+        x_end=_np(out["x_end"][bs, cs]),
+    )
+
+
+def compare_rows(got, ref, io: str) -> Dict[str, float]:
+    return dict(
+        y_prefill=check_y(got["y_prefill"], ref["y_prefill"], io, "prefill y"),
+        y_dec=check_y(got["y_dec"], ref["y_dec"], io, "decode y"),
+        x_T=check_x(got["x_T"], ref["x_T"], "x_T"),
+        x_end=check_x(got["x_end"], ref["x_end"], "x_end"),
+    )
+
+
+def sample_rows(B: int, D: int, n: int, seed: int = 123) -> List[Tuple[int, int]]:
+    rng = np.random.default_rng(seed)
+    rows = {(0, 0), (B - 1, D - 1), (0, D - 1), (B - 1, 0)}
+    while len(rows) < min(n, B * D):
+        rows.add((int(rng.integers(B)), int(rng.integers(D))))
+    return sorted(rows)

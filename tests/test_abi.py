@@ -1,0 +1,166 @@
+"""C ABI checks that need no GPU: the library loads, exports every function
+``include/lh.h`` declares, and rejects bad arguments on the host with the
+documented status before touching any device.
+
+Calls here pass made-up addresses; they are only made where the library
+returns before any device work (argument errors), and the "all arguments
+valid" case runs only when no GPU is visible (it must then report
+LH_ERR_NO_DEVICE).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2310_18780_amd as lh
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "lh.h")
+
+pytestmark = pytest.mark.skipif(not os.path.exists(lh.library_path()),
+                                reason="liblh.so not built (run __graft_entry__.build())")
+
+
+def header_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(lh_[a-z_0-9]+)\s*\(", text)))
+
+
+def header_enum(name):
+    text = open(HEADER).read()
+    m = re.search(r"#define\s+" + name + r"\s+(\d+)", text)
+    return int(m.group(1))
+
+
+def no_gpu():
+    import torch
+
+    return torch.cuda.device_count() == 0
+
+
+def test_exports_every_declared_symbol():
+    L = lh.lib()
+    names = header_functions()
+    assert {"lh_prefill", "lh_step", "lh_prefill_workspace_bytes", "lh_status_string"} <= set(names)
+    for n in names:
+        assert hasattr(L, n), f"{n} declared in lh.h but not exported"
+
+
+def test_exported_symbols_are_c_linkage():
+    out = os.popen(f"nm -D --defined-only {lh.library_path()}").read()
+    for n in header_functions():
+        assert re.search(r"\bT " + n + r"$", out, flags=re.M), n
+
+
+def test_abi_version_and_status_strings():
+    L = lh.lib()
+    assert L.lh_abi_version() == header_enum("LH_ABI_VERSION")
+    for code, name in lh.STATUS.items():
+        assert L.lh_status_string(code).decode().startswith(name)
+    assert L.lh_status_string(99).decode() == "unknown lh_status"
+
+
+def test_workspace_sizes():
+    # no workspace for T = 0 or a single chunk
+    assert lh.workspace_bytes(2, 8, 4, 0) == 0
+    assert lh.workspace_bytes(2, 8, 4, 100, chunk_len=100) == 0
+    assert lh.workspace_bytes(2, 8, 4, 100, chunk_len=500) == 0
+    # chunked: lambda^C table (256-byte aligned) + [B, nchunks, D, d] entry states
+    B, D, d, T, C = 3, 10, 4, 100, 30
+    nch = -(-T // C)
+    pow_bytes = -(-(D * d * 8) // 256) * 256
+    assert lh.workspace_bytes(B, D, d, T, chunk_len=C) == pow_bytes + B * nch * D * d * 8
+    # automatic plan of the long-prompt workload is chunked, of the wide ones not
+    assert lh.workspace_bytes(4, 1024, 32, 65536) > 0
+    assert lh.workspace_bytes(64, 2048, 16, 4096) == 0
+    assert lh.workspace_bytes(256, 2048, 64, 1024) == 0
+    # invalid sizes
+    L = lh.lib()
+    bad = ctypes.c_size_t(-1).value
+    for args in [(0, 1, 1, 1, 0), (1, 0, 1, 1, 0), (1, 1, 0, 1, 0), (1, 1, 1025, 1, 0),
+                 (1, 1, 1, -1, 0), (1, 1, 1, 1, -1), (1 << 40, 1 << 20, 64, 1 << 20, 0)]:
+        assert L.lh_prefill_workspace_bytes(*args) == bad, args
+
+
+# made-up, well-separated, aligned addresses (never dereferenced)
+A = 0x7F0000000000
+MB = 1 << 20
+
+
+def prefill_args(**kw):
+    a = dict(lam=A, R=A + MB, h0=A + 2 * MB, u=A + 3 * MB, B=2, D=8, d=4, T=16, io=lh.LH_F32,
+             state=A + 64 * MB, y=A + 128 * MB, chunk=0, ws=None, ws_bytes=0, stream=None)
+    a.update(kw)
+    return [a[k] for k in ("lam", "R", "h0", "u", "B", "D", "d", "T", "io", "state", "y", "chunk",
+                           "ws", "ws_bytes", "stream")]
+
+
+def step_args(**kw):
+    a = dict(lam=A, R=A + MB, h0=A + 2 * MB, state=A + 64 * MB, u=A + 3 * MB, y=A + 128 * MB,
+             B=2, D=8, d=4, io=lh.LH_F32, stream=None)
+    a.update(kw)
+    return [a[k] for k in ("lam", "R", "h0", "state", "u", "y", "B", "D", "d", "io", "stream")]
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(lam=None), 1), (dict(R=None), 1), (dict(h0=None), 1), (dict(state=None), 1),
+    (dict(u=None), 1), (dict(y=None), 1),
+    (dict(B=0), 1), (dict(D=-3), 1), (dict(d=0), 1), (dict(d=1025), 1), (dict(T=-1), 1),
+    (dict(chunk=-2), 1),
+    (dict(B=1 << 40, D=1 << 20), 1),  # element count overflow
+    (dict(io=7), 3),
+    (dict(u=A + 3 * MB + 2), 1),  # misaligned float32 input
+    (dict(lam=A + 4), 1),  # misaligned complex64
+    (dict(y=A + 3 * MB + 64), 2),  # y overlaps u
+    (dict(state=A + MB + 8), 2),  # state overlaps R
+    (dict(y=A + 64 * MB + 16), 2),  # y overlaps state
+    (dict(chunk=4), 5),  # chunked plan needs a workspace
+    (dict(chunk=4, ws=A + 256 * MB, ws_bytes=16), 5),  # too small
+    (dict(chunk=4, ws=A + 256 * MB + 8, ws_bytes=1 << 20), 1),  # misaligned workspace
+    (dict(chunk=4, ws=A + 64 * MB, ws_bytes=1 << 20), 2),  # workspace overlaps state
+])
+def test_prefill_rejects_bad_arguments(kw, status):
+    L = lh.lib()
+    assert L.lh_prefill(*prefill_args(**kw)) == status
+    assert L.lh_last_error().decode() != ""
+
+
+def test_prefill_t0_allows_null_io():
+    if not no_gpu():
+        pytest.skip("made-up addresses are only passed through when no GPU is visible")
+    L = lh.lib()
+    assert L.lh_prefill(*prefill_args(T=0, u=None, y=None)) == 4  # reaches the device check
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(lam=None), 1), (dict(y=None), 1), (dict(u=None), 1), (dict(state=None), 1),
+    (dict(B=0), 1), (dict(d=2000), 1), (dict(io=2), 3),
+    (dict(y=A + 3 * MB), 2),  # y_t aliases u_t
+    (dict(state=A + 2 * MB), 2),  # state overlaps h0
+    (dict(y=A + 64 * MB + 8), 2),  # y_t overlaps state
+    (dict(h0=A + 2 * MB + 2), 1),
+])
+def test_step_rejects_bad_arguments(kw, status):
+    L = lh.lib()
+    assert L.lh_step(*step_args(**kw)) == status
+
+
+def test_valid_arguments_report_no_device_without_gpu():
+    if not no_gpu():
+        pytest.skip("made-up addresses are only passed through when no GPU is visible")
+    L = lh.lib()
+    assert L.lh_prefill(*prefill_args()) == 4
+    assert "device" in L.lh_last_error().decode()
+    assert L.lh_step(*step_args()) == 4
+    assert L.lh_step(*step_args(io=lh.LH_BF16)) == 4
+
+
+def test_binding_raises_when_library_missing(monkeypatch, tmp_path):
+    monkeypatch.setattr(lh, "_LIB_PATH", str(tmp_path / "missing.so"))
+    monkeypatch.setattr(lh, "_lib", None)
+    with pytest.raises(ImportError):
+        lh.lib()

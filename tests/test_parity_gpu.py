@@ -1,0 +1,242 @@
+"""GPU parity: the HIP path, called through the C ABI, against the CPU oracle
+on the same seeded inputs (tolerances in ``parity_util``).
+
+* small cases: every output and state, over shapes that span several
+  wavefronts, chunks and ragged tails, both I/O dtypes, odd and large mode
+  counts, T = 0, single-step chunks;
+* the five workloads at their full sizes, in the launch configuration the
+  benchmark uses: all outputs and states of sampled (b, c) rows, which the
+  oracle computes one by one;
+* properties that hold at any size: prefill(T) + K steps == prefill(T + K),
+  bitwise determinism, HIP-graph replay == eager, state save / restore.
+"""
+from __future__ import annotations
+
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+import workloads
+from parity_util import (compare_full, compare_rows, gather_rows, run_gpu, sample_rows,
+                         to_device, check_y, check_x, _np)
+
+pytestmark = pytest.mark.gpu
+
+
+def _log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    import torch
+
+    import paper_2310_18780_amd as lh
+
+    assert torch.cuda.is_available(), "GPU tests need a HIP device"
+    lh.lib()  # fails loudly when the library is missing
+    yield
+
+
+def small_case(B, D, d, T, K, io, seed=0, r=(0.5, 0.999), theta=np.pi):
+    w = workloads.Workload("case", B, D, d, T, K, io, r[0], r[1], theta, 1.0 / d, seed)
+    return w, workloads.make_inputs(w)
+
+
+# (B, D, d, T, K, io, chunk_len)
+SMALL = [
+    (1, 4, 4, 64, 16, "f32", 0),       # the tiny workload's shape, automatic plan
+    (2, 70, 16, 300, 20, "f32", 0),    # one sequential pass, D not a multiple of 64
+    (2, 70, 16, 300, 20, "f32", 64),   # chunked, ragged last chunk (300 = 4*64 + 44)
+    (3, 130, 3, 257, 9, "bf16", 32),   # odd d (masked modes), bf16 I/O, ragged
+    (1, 65, 32, 200, 5, "f32", 48),    # two lanes per row
+    (2, 33, 64, 129, 7, "f32", 16),    # four lanes per row
+    (2, 33, 64, 129, 7, "bf16", 0),
+    (1, 7, 1, 100, 3, "f32", 0),       # d = 1
+    (1, 7, 1, 100, 3, "f32", 7),
+    (1, 5, 17, 50, 4, "f32", 8),       # d = 17: 2 lanes x 16 modes, 15 masked
+    (2, 9, 100, 40, 3, "f32", 0),      # d = 100: 8 lanes per row
+    (1, 3, 1024, 20, 2, "f32", 0),     # the largest d: 64 lanes per row
+    (1, 3, 1024, 20, 2, "f32", 6),
+    (1, 4, 6, 64, 4, "f32", 0),        # step: 3 mode pairs per lane
+    (1, 4, 5, 64, 4, "bf16", 0),       # step: single modes, 8 lanes per row
+    (2, 10, 4, 0, 5, "f32", 0),        # T = 0: zero state, decode from zero
+    (2, 10, 4, 1, 3, "f32", 0),        # T = 1
+    (1, 8, 4, 40, 3, "f32", 1),        # every step its own chunk
+    (1, 8, 4, 40, 3, "f32", 39),       # two chunks, last of length 1
+    (4, 256, 16, 512, 8, "bf16", 64),  # many waves, bf16, chunked
+]
+
+
+@pytest.mark.parametrize("case", SMALL, ids=[
+    f"B{c[0]}_D{c[1]}_d{c[2]}_T{c[3]}_K{c[4]}_{c[5]}_C{c[6]}" for c in SMALL])
+def test_small_case(case):
+    B, D, d, T, K, io, chunk = case
+    _log(f"[small] {case}")
+    w, (lam, R, h0, up, ud) = small_case(B, D, d, T, K, io)
+    ref = oracle.run(lam, R, h0, up, ud)
+    out = run_gpu(to_device(lam, R, h0, up, ud, io), chunk_len=chunk)
+    errs = compare_full(out, ref, io)
+    _log(f"[small] {case} max row-relative errors {errs}")
+
+
+def test_tiny_workload():
+    w = workloads.workload("tiny")
+    lam, R, h0, up, ud = workloads.make_inputs(w)
+    ref = oracle.run(lam, R, h0, up, ud)
+    out = run_gpu(to_device(lam, R, h0, up, ud, w.io))
+    _log(f"[tiny] {compare_full(out, ref, w.io)}")
+
+
+@pytest.mark.parametrize("name", ["c2", "c3", "c4", "c5"])
+def test_full_workload_sampled_rows(name):
+    """Full-size workload, automatic plan (as benchmarked): every output and
+    state of sampled (b, c) rows against the oracle."""
+    import torch
+
+    w = workloads.workload(name)
+    _log(f"[full] {w}")
+    lam, R, h0, up, ud = workloads.make_inputs(w)
+    t = to_device(lam, R, h0, up, ud, w.io)
+    out = run_gpu(t)
+    rows = sample_rows(w.B, w.D, 24)
+    got = gather_rows(out, rows)
+    del out, t
+    torch.cuda.empty_cache()
+    ref = oracle.run_rows(lam, R, h0, up, ud, rows)
+    _log(f"[full] {name} rows={len(rows)} errors {compare_rows(got, ref, w.io)}")
+
+
+@pytest.mark.parametrize("name", ["c2", "c3", "c5"])
+def test_decode_continues_prefill(name):
+    """prefill(T) followed by K steps gives the outputs and state of a single
+    prefill over the T + K inputs (any size; GPU against GPU)."""
+    import torch
+
+    import paper_2310_18780_amd as lh
+
+    w = workloads.workload(name)
+    if name == "c5":
+        w = w.with_(T=8192)  # keep the concatenated copy small
+    lam, R, h0, up, ud = workloads.make_inputs(w)
+    t = to_device(lam, R, h0, up, ud, w.io)
+    out = run_gpu(t)
+    ucat = torch.cat([t["u"], t["ud"].transpose(0, 1)], dim=1).contiguous()
+    y2 = torch.empty_like(ucat)
+    st2 = torch.empty_like(out["x_end"])
+    lh.prefill(t["lam"], t["R"], t["h0"], ucat, st2, y2)
+    torch.cuda.synchronize()
+    B, D, d = w.B, w.D, w.d
+    yd = _np(out["y_dec"]).transpose(1, 2, 0).reshape(B * D, -1)
+    y2d = _np(y2[:, w.T:]).transpose(0, 2, 1).reshape(B * D, -1).astype(np.float64)
+    check_y(yd, y2d, w.io, "decode vs long prefill", ref_rounded=True)
+    check_x(_np(out["x_end"]).reshape(-1, d), _np(st2).reshape(-1, d).astype(np.complex128),
+            "state after decode vs long prefill")
+
+
+def _bits(x):
+    import torch
+
+    if x.is_complex():
+        x = torch.view_as_real(x)
+    return x.contiguous().view(torch.int16 if x.element_size() == 2 else torch.int32)
+
+
+def test_bitwise_determinism():
+    """Two runs on the same inputs give identical bits (the kernels use no
+    atomics and a fixed reduction order)."""
+    import torch
+
+    w = workloads.workload("c2")
+    lam, R, h0, up, ud = workloads.make_inputs(w.with_(K=32))
+    t = to_device(lam, R, h0, up, ud, w.io)
+    for chunk in (0, 100):
+        a = run_gpu(t, chunk_len=chunk)
+        b = run_gpu(t, chunk_len=chunk)
+        for k in a:
+            assert torch.equal(_bits(a[k]), _bits(b[k])), (chunk, k)
+
+
+def test_graph_replay_matches_eager():
+    """K decode steps (and a prefill) captured in a HIP graph; every replay,
+    with eager work in between, equals the eager run bit for bit."""
+    import torch
+
+    import paper_2310_18780_amd as lh
+
+    w = workloads.workload("c3").with_(B=8, T=256, K=24)
+    lam, R, h0, up, ud = workloads.make_inputs(w)
+    t = to_device(lam, R, h0, up, ud, w.io)
+    eager = run_gpu(t)
+
+    B, T, D, d, K = w.B, w.T, w.D, w.d, w.K
+    y = torch.empty_like(t["u"])
+    state = torch.empty((B, D, d), dtype=torch.complex64, device="cuda")
+    y_dec = torch.empty((K, B, D), dtype=t["u"].dtype, device="cuda")
+    x_T = torch.empty_like(state)
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):  # warm-up on a side stream before capture
+        lh.prefill(t["lam"], t["R"], t["h0"], t["u"], state, y)
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        lh.prefill(t["lam"], t["R"], t["h0"], t["u"], state, y)
+        x_T.copy_(state)
+        for k in range(K):
+            lh.step(t["lam"], t["R"], t["h0"], state, t["ud"][k], y_dec[k])
+    for rep in range(4):
+        y.fill_(float("nan"))
+        y_dec.fill_(float("nan"))
+        state.fill_(0)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        junk = torch.randn(1 << 20, device="cuda").sum()  # unrelated eager work
+        torch.cuda.synchronize()
+        assert torch.equal(y, eager["y_prefill"]), rep
+        assert torch.equal(x_T, eager["x_T"]), rep
+        assert torch.equal(y_dec, eager["y_dec"]), rep
+        assert torch.equal(state, eager["x_end"]), rep
+        del junk
+
+
+def test_state_save_restore():
+    """The state is the checkpoint: copy it to the host mid-decode, restore it
+    into a fresh buffer and continue; outputs are bitwise identical."""
+    import torch
+
+    import paper_2310_18780_amd as lh
+
+    w = workloads.workload("c2").with_(K=40)
+    lam, R, h0, up, ud = workloads.make_inputs(w)
+    t = to_device(lam, R, h0, up, ud, w.io)
+    ref = run_gpu(t)
+    state = torch.empty((w.B, w.D, w.d), dtype=torch.complex64, device="cuda")
+    y = torch.empty_like(t["u"])
+    lh.prefill(t["lam"], t["R"], t["h0"], t["u"], state, y)
+    yk = torch.empty((w.B, w.D), dtype=t["u"].dtype, device="cuda")
+    for k in range(17):
+        lh.step(t["lam"], t["R"], t["h0"], state, t["ud"][k], yk)
+    host = state.cpu()
+    del state
+    fresh = host.to("cuda")
+    for k in range(17, w.K):
+        lh.step(t["lam"], t["R"], t["h0"], fresh, t["ud"][k], yk)
+        assert torch.equal(yk, ref["y_dec"][k]), k
+    assert torch.equal(fresh, ref["x_end"])
+
+
+def test_chunk_plans_agree_with_oracle_on_long_prompt():
+    """The long-prompt poles (r up to 0.99999, near-DC) over 16k steps with
+    several explicit chunk lengths, all rows checked."""
+    w = workloads.workload("c5").with_(B=1, D=96, T=16384, K=8)
+    lam, R, h0, up, ud = workloads.make_inputs(w)
+    ref = oracle.run(lam, R, h0, up, ud)
+    t = to_device(lam, R, h0, up, ud, w.io)
+    for chunk in (0, 256, 1000, 4096, 16384):
+        out = run_gpu(t, chunk_len=chunk)
+        _log(f"[long] chunk={chunk} {compare_full(out, ref, w.io)}")

@@ -104,13 +104,14 @@ def workload(name: str) -> Workload:
 
 def bf16_round(x: np.ndarray) -> np.ndarray:
     """Round float32 values to the nearest bfloat16 (ties to even); returns
-    float32 values that are exactly representable in bfloat16.  NaN stays NaN."""
+    float32 values that are exactly representable in bfloat16.  NaN stays NaN.
+    (For finite inputs and infinities the uint32 sum below cannot wrap.)"""
     x = np.ascontiguousarray(x, dtype=np.float32)
-    bits = x.view(np.uint32).astype(np.uint64)
-    lsb = (bits >> 16) & 1
-    rounded = ((bits + 0x7FFF + lsb) >> 16) << 16
-    out = rounded.astype(np.uint32).view(np.float32)
-    return np.where(np.isnan(x), x, out).astype(np.float32)
+    bits = x.view(np.uint32)
+    lsb = (bits >> np.uint32(16)) & np.uint32(1)
+    rounded = (bits + (np.uint32(0x7FFF) + lsb)) & np.uint32(0xFFFF0000)
+    out = rounded.view(np.float32)
+    return np.where(np.isnan(x), x, out)
 
 
 def bf16_bits(x: np.ndarray) -> np.ndarray:
