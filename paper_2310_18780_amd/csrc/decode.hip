@@ -5,16 +5,27 @@
 //   x[b,c,n]    <- lambda[c,n] x[b,c,n] + u[b,c]          (in place)
 //
 // One pass over the [B, D, d] complex64 state: read once, written once, so the
-// kernel is bound by HBM bandwidth (about 16 bytes of state traffic per mode
-// against 12 flops).  The d modes of a (b, c) row are spread over LPR
-// consecutive lanes (VEC = 2: pairs of adjacent modes per access), so that a wave
-// reads and writes one contiguous span of the state with 8- or 16-byte
-// accesses; the per-row sum is a butterfly over those lanes.
+// kernel is bound by memory bandwidth (16 bytes of state traffic per mode
+// against 12 flops).
 //
-// Blocks are mapped XCD-aware: hardware workgroup i runs on XCD (i mod 8), so
-// the logical block index is permuted to give each XCD a contiguous range of
-// channel tiles.  A tile's lambda/R (shared by all batch rows) then stays in
-// that XCD's L2 instead of being fetched by all eight.
+// Fast path (d even, d/2 a power of two <= 128, 16-byte aligned arrays): the
+// d/2 mode pairs of a (b, c) row sit on LPR = d/2 consecutive lanes, one
+// 16-byte access each, so a wavefront reads and writes one contiguous span of
+// the state; the row sum is a butterfly over those lanes.  Each thread serves
+// NB = 4 batch rows of the same (c, mode pair): lambda and R are loaded once
+// for the four rows, and every thread has four independent 16-byte state loads
+// in flight before it computes.  Two memory policies, chosen by state size:
+//
+//  * resident (state < 128 MiB, can stay in the 256 MB Infinity Cache between
+//    steps): ordinary loads, non-temporal stores, consecutive workgroups on the
+//    same channel tile;
+//  * streaming (larger states): non-temporal loads and stores, consecutive
+//    workgroups on consecutive channel tiles with the tile count padded to a
+//    multiple of 8, so that (workgroup i runs on XCD i mod 8) every channel
+//    tile and its lambda/R stay on one XCD.
+//
+// Generic path (any other d): lanes take single modes j, j + LPR, ...
+// (LPR = next power of two >= d, <= 64) or pairs, one batch row per thread.
 #include "lh_internal.hpp"
 
 namespace lh {
@@ -22,65 +33,132 @@ namespace {
 
 constexpr int kBlock = 256;
 constexpr int kXcds = 8;
+constexpr int kRowsPerThread = 4;
+constexpr int64_t kResidentStateBytes = int64_t(128) << 20;
 
-__device__ __forceinline__ int64_t xcd_logical_block(int64_t hw, int64_t nblocks) {
-    // hardware block hw -> XCD (hw % 8), k-th block of that XCD; XCD x owns
-    // logical blocks [x * per, (x + 1) * per).
-    const int64_t per = (nblocks + kXcds - 1) / kXcds;
-    const int64_t x = hw % kXcds;
-    const int64_t k = hw / kXcds;
-    return x * per + k;
+typedef float f4v __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ float4 load4(const float2* p, bool nt)
+{
+    const f4v* q = reinterpret_cast<const f4v*>(p);
+    const f4v v = nt ? __builtin_nontemporal_load(q) : *q;
+    return make_float4(v.x, v.y, v.z, v.w);
 }
 
-// VEC = 2: each lane owns NI pairs of modes (16-byte accesses); requires
-// d % (2 * LPR) == 0.  VEC = 1: each lane owns modes j, j + LPR, ... (8-byte
-// accesses), any d.
-template <typename IO, int LPR, int VEC>
-__global__ __launch_bounds__(kBlock) void step_kernel(
-    const float2* __restrict__ lam, const float2* __restrict__ R, const float* __restrict__ h0,
-    float2* __restrict__ state, const IO* __restrict__ u, IO* __restrict__ y,
-    int64_t B, int64_t D, int64_t d, int64_t nblocks)
+__device__ __forceinline__ void store4(float2* p, float4 a, bool nt)
 {
-    constexpr int kRows = kBlock / LPR;  // rows (channels) per block
-    const int64_t lb = xcd_logical_block(blockIdx.x, nblocks);
+    f4v* q = reinterpret_cast<f4v*>(p);
+    const f4v v = {a.x, a.y, a.z, a.w};
+    if (nt)
+        __builtin_nontemporal_store(v, q);
+    else
+        *q = v;
+}
+
+// complex multiply-add of two modes held as (re0, im0, re1, im1)
+__device__ __forceinline__ float4 step_pair(float4 l, float4 x, float uv)
+{
+    float4 n;
+    n.x = fmaf(l.x, x.x, fmaf(-l.y, x.y, uv));
+    n.y = fmaf(l.x, x.y, l.y * x.x);
+    n.z = fmaf(l.z, x.z, fmaf(-l.w, x.w, uv));
+    n.w = fmaf(l.z, x.w, l.w * x.z);
+    return n;
+}
+
+__device__ __forceinline__ float re_dot_pair(float4 r, float4 x)
+{
+    return fmaf(r.x, x.x, fmaf(-r.y, x.y, fmaf(r.z, x.z, -r.w * x.w)));
+}
+
+// Fast path: LPR = d / 2 lanes per row, NB rows per thread, 2-D grid of
+// (channel tile, batch group) blocks, so no integer division is needed to
+// place a block.  Resident policy: blockIdx.x = batch group (consecutive
+// blocks share a channel tile), plain loads, non-temporal stores.  Streaming
+// policy: blockIdx.x = channel tile with gridDim.x a multiple of 8, so each
+// channel tile (and its lambda/R) lives on one XCD for all batch groups;
+// non-temporal loads and stores.
+template <typename IO, int LPR, bool STREAM>
+__global__ __launch_bounds__(kBlock) void step_pairs_kernel(
+    const float2* __restrict__ lam, const float2* __restrict__ R, const float* __restrict__ h0,
+    float2* __restrict__ state, const IO* __restrict__ u, IO* __restrict__ y, int B, int D,
+    int ntiles)
+{
+    constexpr int NB = kRowsPerThread;
+    constexpr int kRows = kBlock / LPR;  // channels per block
+    constexpr int d = 2 * LPR;
+    const int ct = STREAM ? blockIdx.x : blockIdx.y;  // channel tile
+    const int b0 = (STREAM ? blockIdx.y : blockIdx.x) * NB;
+    if (ct >= ntiles) return;  // padding tiles of the streaming grid
+    const int j = threadIdx.x % LPR;
+    const int c = ct * kRows + threadIdx.x / LPR;
+    const bool cvalid = c < D;
+    const int cc = cvalid ? c : D - 1;  // every address stays in bounds
+
+    const float4 l4 = load4(lam + int64_t(cc) * d + 2 * j, false);
+    const float4 r4 = load4(R + int64_t(cc) * d + 2 * j, false);
+    float4 x[NB];
+    float uv[NB];
+#pragma unroll
+    for (int i = 0; i < NB; ++i) {
+        const int b = (b0 + i < B) ? b0 + i : B - 1;
+        const int64_t row = int64_t(b) * D + cc;
+        x[i] = load4(state + row * d + 2 * j, STREAM);
+        uv[i] = io_load(u + row);
+    }
+    const float hz = h0[cc];
+#pragma unroll
+    for (int i = 0; i < NB; ++i) {
+        const int b = b0 + i;
+        float acc = re_dot_pair(r4, x[i]);
+        const float4 n4 = step_pair(l4, x[i], uv[i]);
+#pragma unroll
+        for (int off = 1; off < LPR; off <<= 1) acc += __shfl_xor(acc, off, LPR);
+        if (cvalid && b < B) {
+            const int64_t row = int64_t(b) * D + c;
+            store4(state + row * d + 2 * j, n4, true);
+            if (j == 0) io_store(y + row, fmaf(hz, uv[i], acc));
+        }
+    }
+}
+
+// Generic path.  VEC = 2: each lane owns pairs m = 2 (j + i LPR), requires
+// d % (2 LPR) == 0 and 16-byte alignment; VEC = 1: modes j, j + LPR, ...
+template <typename IO, int LPR, int VEC>
+__global__ __launch_bounds__(kBlock) void step_generic_kernel(
+    const float2* __restrict__ lam, const float2* __restrict__ R, const float* __restrict__ h0,
+    float2* __restrict__ state, const IO* __restrict__ u, IO* __restrict__ y, int64_t B,
+    int64_t D, int64_t d, int64_t nblocks)
+{
+    constexpr int kRows = kBlock / LPR;
+    const int64_t lb = blockIdx.x;
     if (lb >= nblocks) return;
-    const int64_t ct = lb / B;  // channel tile
+    const int64_t ct = lb / B;
     const int64_t b = lb - ct * B;
     const int j = threadIdx.x % LPR;
     const int64_t c = ct * kRows + threadIdx.x / LPR;
     const bool valid = c < D;
-    const int64_t cc = valid ? c : D - 1;  // keep every address in bounds
+    const int64_t cc = valid ? c : D - 1;
 
     const float uv = io_load(u + b * D + cc);
     const float2* lrow = lam + cc * d;
     const float2* rrow = R + cc * d;
     float2* xrow = state + (b * D + cc) * d;
-
     float acc = 0.f;
     if constexpr (VEC == 2) {
         const int64_t ni = d / (2 * LPR);
         for (int64_t i = 0; i < ni; ++i) {
             const int64_t m = 2 * (j + i * LPR);
-            const float4 l4 = *reinterpret_cast<const float4*>(lrow + m);
-            const float4 r4 = *reinterpret_cast<const float4*>(rrow + m);
-            const float4 x4 = valid ? *reinterpret_cast<const float4*>(xrow + m)
-                                    : make_float4(0.f, 0.f, 0.f, 0.f);
-            acc = fmaf(r4.x, x4.x, acc);
-            acc = fmaf(-r4.y, x4.y, acc);
-            acc = fmaf(r4.z, x4.z, acc);
-            acc = fmaf(-r4.w, x4.w, acc);
-            float4 n4;
-            n4.x = fmaf(l4.x, x4.x, fmaf(-l4.y, x4.y, uv));
-            n4.y = fmaf(l4.x, x4.y, l4.y * x4.x);
-            n4.z = fmaf(l4.z, x4.z, fmaf(-l4.w, x4.w, uv));
-            n4.w = fmaf(l4.z, x4.w, l4.w * x4.z);
-            if (valid) *reinterpret_cast<float4*>(xrow + m) = n4;
+            const float4 x4 = load4(xrow + m, false);
+            acc += re_dot_pair(load4(rrow + m, false), x4);
+            const float4 n4 = step_pair(load4(lrow + m, false), x4, uv);
+            if (valid) store4(xrow + m, n4, false);
         }
     } else {
         for (int64_t m = j; m < d; m += LPR) {
             const float2 l2 = lrow[m];
             const float2 r2 = rrow[m];
-            const float2 x2 = valid ? xrow[m] : make_float2(0.f, 0.f);
+            const float2 x2 = xrow[m];
             acc = fmaf(r2.x, x2.x, acc);
             acc = fmaf(-r2.y, x2.y, acc);
             float2 n2;
@@ -94,36 +172,84 @@ __global__ __launch_bounds__(kBlock) void step_kernel(
     if (valid && j == 0) io_store(y + b * D + c, fmaf(h0[c], uv, acc));
 }
 
-template <typename IO, int VEC>
-hipError_t launch_lpr(int lpr, const float2* lam, const float2* R, const float* h0,
-                      float2* state, const void* u, void* y, int64_t B, int64_t D, int64_t d,
-                      hipStream_t stream)
+// 2-D grid of the fast path; false when it does not fit the grid limits
+bool pairs_grid(int lpr, bool stream_policy, int64_t B, int64_t D, dim3* g, int* ntiles)
 {
     const int64_t rows_per_block = kBlock / lpr;
-    const int64_t ntiles = (D + rows_per_block - 1) / rows_per_block;
-    const int64_t nblocks = ntiles * B;
-    const int64_t grid = ((nblocks + kXcds - 1) / kXcds) * kXcds;  // every XCD gets `per` slots
-    if (grid > 0x7fffffff) return hipErrorInvalidConfiguration;
+    const int64_t nt = (D + rows_per_block - 1) / rows_per_block;
+    const int64_t nbg = (B + kRowsPerThread - 1) / kRowsPerThread;
+    const int64_t ntp = (nt + kXcds - 1) / kXcds * kXcds;
+    if (stream_policy) {
+        if (ntp > 0x7fffffff || nbg > 65535) return false;
+        *g = dim3(uint32_t(ntp), uint32_t(nbg));
+    } else {
+        if (nbg > 0x7fffffff || nt > 65535) return false;
+        *g = dim3(uint32_t(nbg), uint32_t(nt));
+    }
+    *ntiles = int(nt);
+    return true;
+}
+
+template <typename IO>
+hipError_t launch_pairs(int lpr, bool stream_policy, dim3 grid, int ntiles, const float2* lam,
+                        const float2* R, const float* h0, float2* state, const void* u, void* y,
+                        int64_t B, int64_t D, hipStream_t stream)
+{
     const IO* uu = static_cast<const IO*>(u);
     IO* yy = static_cast<IO*>(y);
-#define LH_STEP_CASE(L)                                                                   \
-    case L:                                                                               \
-        hipLaunchKernelGGL((step_kernel<IO, L, VEC>), dim3(static_cast<uint32_t>(grid)), \
-                           dim3(kBlock), 0, stream, lam, R, h0, state, uu, yy, B, D, d,   \
-                           nblocks);                                                      \
+    const int b = int(B), dd = int(D);
+#define LH_PAIRS(L)                                                                            \
+    case L:                                                                                    \
+        if (stream_policy)                                                                     \
+            hipLaunchKernelGGL((step_pairs_kernel<IO, L, true>), grid, dim3(kBlock), 0, stream, \
+                               lam, R, h0, state, uu, yy, b, dd, ntiles);                      \
+        else                                                                                   \
+            hipLaunchKernelGGL((step_pairs_kernel<IO, L, false>), grid, dim3(kBlock), 0,       \
+                               stream, lam, R, h0, state, uu, yy, b, dd, ntiles);              \
         break;
     switch (lpr) {
-        LH_STEP_CASE(1)
-        LH_STEP_CASE(2)
-        LH_STEP_CASE(4)
-        LH_STEP_CASE(8)
-        LH_STEP_CASE(16)
-        LH_STEP_CASE(32)
-        LH_STEP_CASE(64)
+        LH_PAIRS(1)
+        LH_PAIRS(2)
+        LH_PAIRS(4)
+        LH_PAIRS(8)
+        LH_PAIRS(16)
+        LH_PAIRS(32)
+        LH_PAIRS(64)
         default:
             return hipErrorInvalidValue;
     }
-#undef LH_STEP_CASE
+#undef LH_PAIRS
+    return hipGetLastError();
+}
+
+template <typename IO, int VEC>
+hipError_t launch_generic(int lpr, const float2* lam, const float2* R, const float* h0,
+                          float2* state, const void* u, void* y, int64_t B, int64_t D, int64_t d,
+                          hipStream_t stream)
+{
+    const int64_t rows_per_block = kBlock / lpr;
+    const int64_t nblocks = (D + rows_per_block - 1) / rows_per_block * B;
+    if (nblocks > 0x7fffffff) return hipErrorInvalidConfiguration;
+    const IO* uu = static_cast<const IO*>(u);
+    IO* yy = static_cast<IO*>(y);
+#define LH_GEN(L)                                                                            \
+    case L:                                                                                  \
+        hipLaunchKernelGGL((step_generic_kernel<IO, L, VEC>), dim3(uint32_t(nblocks)),       \
+                           dim3(kBlock), 0, stream, lam, R, h0, state, uu, yy, B, D, d,      \
+                           nblocks);                                                         \
+        break;
+    switch (lpr) {
+        LH_GEN(1)
+        LH_GEN(2)
+        LH_GEN(4)
+        LH_GEN(8)
+        LH_GEN(16)
+        LH_GEN(32)
+        LH_GEN(64)
+        default:
+            return hipErrorInvalidValue;
+    }
+#undef LH_GEN
     return hipGetLastError();
 }
 
@@ -133,25 +259,32 @@ hipError_t launch_step(const float2* lam, const float2* R, const float* h0, floa
                        const void* u_t, void* y_t, bool bf16_io, int64_t B, int64_t D,
                        int64_t d, bool aligned16, hipStream_t stream)
 {
-    // Lane layout: with d even (and 16-byte aligned arrays), lanes take pairs
-    // of modes (16-byte accesses) and LPR is the largest power of two dividing
-    // d / 2, capped at 32; otherwise LPR is the next power of two >= d, capped
-    // at 64, and lanes take single modes.
-    int lpr = 1;
-    const bool vec2 = (d % 2) == 0 && aligned16;
-    if (vec2) {
-        const int64_t pairs = d / 2;
-        while (lpr < 32 && pairs % (2 * lpr) == 0) lpr *= 2;
-    } else {
-        while (lpr < 64 && lpr < d) lpr *= 2;
-    }
     (void)hipGetLastError();  // clear a stale error so the status below is this launch's
-    if (vec2) {
-        return bf16_io ? launch_lpr<bf16, 2>(lpr, lam, R, h0, state, u_t, y_t, B, D, d, stream)
-                       : launch_lpr<float, 2>(lpr, lam, R, h0, state, u_t, y_t, B, D, d, stream);
+    const int64_t pairs = d / 2;
+    const bool pow2_pairs = d % 2 == 0 && pairs >= 1 && pairs <= 64 && (pairs & (pairs - 1)) == 0;
+    dim3 grid;
+    int ntiles = 0;
+    const bool stream_policy = 8 * B * D * d >= kResidentStateBytes;
+    const int fast_lpr = static_cast<int>(pairs);
+    if (pow2_pairs && aligned16 && B < (INT64_C(1) << 31) && D < (INT64_C(1) << 31) &&
+        pairs_grid(fast_lpr, stream_policy, B, D, &grid, &ntiles)) {
+        return bf16_io ? launch_pairs<bf16>(fast_lpr, stream_policy, grid, ntiles, lam, R, h0,
+                                            state, u_t, y_t, B, D, stream)
+                       : launch_pairs<float>(fast_lpr, stream_policy, grid, ntiles, lam, R, h0,
+                                             state, u_t, y_t, B, D, stream);
     }
-    return bf16_io ? launch_lpr<bf16, 1>(lpr, lam, R, h0, state, u_t, y_t, B, D, d, stream)
-                   : launch_lpr<float, 1>(lpr, lam, R, h0, state, u_t, y_t, B, D, d, stream);
+    // generic layouts
+    int lpr = 1;
+    const bool vec2 = d % 2 == 0 && aligned16;
+    if (vec2) {
+        while (lpr < 32 && pairs % (2 * lpr) == 0) lpr *= 2;
+        return bf16_io ? launch_generic<bf16, 2>(lpr, lam, R, h0, state, u_t, y_t, B, D, d, stream)
+                       : launch_generic<float, 2>(lpr, lam, R, h0, state, u_t, y_t, B, D, d,
+                                                  stream);
+    }
+    while (lpr < 64 && lpr < d) lpr *= 2;
+    return bf16_io ? launch_generic<bf16, 1>(lpr, lam, R, h0, state, u_t, y_t, B, D, d, stream)
+                   : launch_generic<float, 1>(lpr, lam, R, h0, state, u_t, y_t, B, D, d, stream);
 }
 
 }  // namespace lh

@@ -18,17 +18,10 @@ __device__ __forceinline__ float io_load(const bf16* p) {
     return __uint_as_float(static_cast<uint32_t>(p->bits) << 16);
 }
 __device__ __forceinline__ void io_store(float* p, float v) { *p = v; }
-// float32 -> bfloat16, round to nearest, ties to even; NaN stays a quiet NaN.
+// float32 -> bfloat16, round to nearest, ties to even (gfx950 converts with
+// one v_cvt_pk_bf16_f32; NaN stays NaN).
 __device__ __forceinline__ void io_store(bf16* p, float v) {
-    uint32_t x = __float_as_uint(v);
-    uint16_t r;
-    if ((x & 0x7fffffffu) > 0x7f800000u) {
-        r = static_cast<uint16_t>((x >> 16) | 0x0040u);
-    } else {
-        x += 0x7fffu + ((x >> 16) & 1u);
-        r = static_cast<uint16_t>(x >> 16);
-    }
-    p->bits = r;
+    p->bits = __builtin_bit_cast(uint16_t, static_cast<__bf16>(v));
 }
 
 // How the prefill of one call is cut up.

@@ -22,7 +22,9 @@
 // cblk * CW + (l % CW) and modes [(l / CW) * MPL, (l / CW + 1) * MPL).  Every
 // time step a wave therefore reads (and writes) one contiguous run of CW
 // channels of u (y), and the LPR mode groups of a row are combined with a
-// butterfly over lanes CW apart.  Inputs are prefetched kPf steps ahead.
+// butterfly over lanes CW apart.  Inputs are prefetched kPf steps ahead; the
+// main loop carries no bounds checks (the channel index is clamped for lanes
+// past D, whose results are discarded), a short tail loop finishes the chunk.
 #include "lh_internal.hpp"
 
 namespace lh {
@@ -30,7 +32,7 @@ namespace {
 
 constexpr int kBlock = 256;
 constexpr int kWavesPerBlock = kBlock / 64;
-constexpr int kPf = 8;  // prefetch depth (time steps)
+constexpr int kPf = 16;  // prefetch depth (time steps)
 
 // ---------------------------------------------------------------- pow kernel
 __global__ __launch_bounds__(kBlock) void pow_kernel(const float2* __restrict__ lam,
@@ -92,6 +94,32 @@ __global__ __launch_bounds__(kBlock) void zero_kernel(float2* __restrict__ p, in
 //                 end state written to xs slot k.
 // OUTPUT = true : output pass over chunks 0 .. nchunks-1, from xs slot k (or 0
 //                 when nchunks == 1), writes y; the last chunk writes state.
+template <int MPL, bool OUTPUT>
+struct Modes {
+    float lr[MPL], li[MPL], rr[MPL], ri[MPL], xr[MPL], xi[MPL];
+
+    // Re(sum_n R_n x_n) over this lane's modes (two chains for ILP)
+    __device__ __forceinline__ float re_rx() const {
+        float a0 = 0.f, a1 = 0.f;
+#pragma unroll
+        for (int m = 0; m < MPL; ++m) {
+            a0 = fmaf(rr[m], xr[m], a0);
+            a1 = fmaf(ri[m], xi[m], a1);
+        }
+        return a0 - a1;
+    }
+    // x <- lambda x + u
+    __device__ __forceinline__ void advance(float uv) {
+#pragma unroll
+        for (int m = 0; m < MPL; ++m) {
+            const float nr = fmaf(lr[m], xr[m], fmaf(-li[m], xi[m], uv));
+            const float ni = fmaf(lr[m], xi[m], li[m] * xr[m]);
+            xr[m] = nr;
+            xi[m] = ni;
+        }
+    }
+};
+
 template <typename IO, int LPR, int MPL, bool OUTPUT>
 __global__ __launch_bounds__(kBlock) void chunk_scan_kernel(
     const float2* __restrict__ lam, const float2* __restrict__ R, const float* __restrict__ h0,
@@ -112,78 +140,79 @@ __global__ __launch_bounds__(kBlock) void chunk_scan_kernel(
 
     const int64_t c = cblk * CW + (lane % CW);
     const bool valid = c < D;
-    const int64_t cc = valid ? c : D - 1;
+    const int64_t cc = valid ? c : D - 1;  // all loads stay in bounds
     const int grp = lane / CW;
     const int64_t n0 = static_cast<int64_t>(grp) * MPL;
-
-    float lr[MPL], li[MPL], rr[MPL], ri[MPL], xr[MPL], xi[MPL];
     const int64_t Dd = D * d;
+
+    Modes<MPL, OUTPUT> md;
 #pragma unroll
     for (int m = 0; m < MPL; ++m) {
         const int64_t n = n0 + m;
-        const bool mv = valid && n < d;
+        const bool mv = n < d;
         const float2 l2 = mv ? lam[cc * d + n] : make_float2(0.f, 0.f);
-        lr[m] = l2.x;
-        li[m] = l2.y;
+        md.lr[m] = l2.x;
+        md.li[m] = l2.y;
+        md.rr[m] = md.ri[m] = md.xr[m] = md.xi[m] = 0.f;
         if constexpr (OUTPUT) {
             const float2 r2 = mv ? R[cc * d + n] : make_float2(0.f, 0.f);
-            rr[m] = r2.x;
-            ri[m] = r2.y;
-            const float2 x2 = (mv && nchunks > 1) ? xs[(b * nchunks + k) * Dd + cc * d + n]
-                                                 : make_float2(0.f, 0.f);
-            xr[m] = x2.x;
-            xi[m] = x2.y;
-        } else {
-            rr[m] = ri[m] = 0.f;
-            xr[m] = xi[m] = 0.f;
+            md.rr[m] = r2.x;
+            md.ri[m] = r2.y;
+            if (mv && nchunks > 1) {
+                const float2 x2 = xs[(b * nchunks + k) * Dd + cc * d + n];
+                md.xr[m] = x2.x;
+                md.xi[m] = x2.y;
+            }
         }
     }
     const float hz = OUTPUT ? h0[cc] : 0.f;
 
     const int64_t t0 = k * C;
-    const int64_t t1 = (t0 + C < T) ? t0 + C : T;
-    const IO* up = u + b * T * D + cc;
-    IO* yp = y + b * T * D + cc;
+    const int64_t n = ((t0 + C < T) ? t0 + C : T) - t0;  // steps of this chunk, wave-uniform
+    const IO* up = u + (b * T + t0) * D + cc;
+    IO* yp = y + (b * T + t0) * D + cc;
 
-    float ub[kPf];
+    auto one_step = [&](float uv, IO* yt) {
+        if constexpr (OUTPUT) {
+            float acc = md.re_rx();
 #pragma unroll
-    for (int s = 0; s < kPf; ++s)
-        ub[s] = (valid && t0 + s < t1) ? io_load(up + (t0 + s) * D) : 0.f;
+            for (int off = CW; off < 64; off <<= 1) acc += __shfl_xor(acc, off, 64);
+            // Every lane stores: lanes of one row hold bit-identical sums (the
+            // butterfly adds commute at each level) and lanes past D repeat
+            // channel D-1 exactly, so duplicate stores write the same value.
+            io_store(yt, fmaf(hz, uv, acc));
+        }
+        md.advance(uv);
+    };
 
-    for (int64_t tb = t0; tb < t1; tb += kPf) {
-        float un[kPf];
+    int64_t t = 0;
+    if (n >= 2 * kPf) {
+        // main loop: block t computed while block t + kPf is in flight
+        float ub[kPf];
 #pragma unroll
-        for (int s = 0; s < kPf; ++s) {
-            const int64_t t = tb + kPf + s;
-            un[s] = (valid && t < t1) ? io_load(up + t * D) : 0.f;
+        for (int s = 0; s < kPf; ++s) ub[s] = io_load(up + s * D);
+        for (; t + 2 * kPf <= n; t += kPf) {
+            float un[kPf];
+#pragma unroll
+            for (int s = 0; s < kPf; ++s) un[s] = io_load(up + (kPf + s) * D);
+#pragma unroll
+            for (int s = 0; s < kPf; ++s) one_step(ub[s], yp + s * D);
+#pragma unroll
+            for (int s = 0; s < kPf; ++s) ub[s] = un[s];
+            up += kPf * D;
+            yp += kPf * D;
         }
+        // block t is loaded (t + kPf <= n)
 #pragma unroll
-        for (int s = 0; s < kPf; ++s) {
-            if (tb + s < t1) {  // wave-uniform
-                const float uv = ub[s];
-                if constexpr (OUTPUT) {
-                    float a0 = 0.f, a1 = 0.f;
-#pragma unroll
-                    for (int m = 0; m < MPL; ++m) {
-                        a0 = fmaf(rr[m], xr[m], a0);
-                        a1 = fmaf(ri[m], xi[m], a1);
-                    }
-                    float acc = a0 - a1;
-#pragma unroll
-                    for (int off = CW; off < 64; off <<= 1) acc += __shfl_xor(acc, off, 64);
-                    if (valid && grp == 0) io_store(yp + (tb + s) * D, fmaf(hz, uv, acc));
-                }
-#pragma unroll
-                for (int m = 0; m < MPL; ++m) {
-                    const float nr = fmaf(lr[m], xr[m], fmaf(-li[m], xi[m], uv));
-                    const float ni = fmaf(lr[m], xi[m], li[m] * xr[m]);
-                    xr[m] = nr;
-                    xi[m] = ni;
-                }
-            }
-        }
-#pragma unroll
-        for (int s = 0; s < kPf; ++s) ub[s] = un[s];
+        for (int s = 0; s < kPf; ++s) one_step(ub[s], yp + s * D);
+        t += kPf;
+        up += kPf * D;
+        yp += kPf * D;
+    }
+    for (; t < n; ++t) {  // tail (< 2 kPf steps)
+        one_step(io_load(up), yp);
+        up += D;
+        yp += D;
     }
 
     // end state: s_k (state pass) or x_T (last chunk of the output pass)
@@ -193,11 +222,11 @@ __global__ __launch_bounds__(kBlock) void chunk_scan_kernel(
     } else {
         dst = xs + (b * nchunks + k) * Dd + cc * d;
     }
-    if (dst != nullptr) {
+    if (dst != nullptr && valid) {
 #pragma unroll
         for (int m = 0; m < MPL; ++m) {
-            const int64_t n = n0 + m;
-            if (valid && n < d) dst[n] = make_float2(xr[m], xi[m]);
+            const int64_t nn = n0 + m;
+            if (nn < d) dst[nn] = make_float2(md.xr[m], md.xi[m]);
         }
     }
 }

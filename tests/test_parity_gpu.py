@@ -67,6 +67,8 @@ SMALL = [
     (1, 8, 4, 40, 3, "f32", 1),        # every step its own chunk
     (1, 8, 4, 40, 3, "f32", 39),       # two chunks, last of length 1
     (4, 256, 16, 512, 8, "bf16", 64),  # many waves, bf16, chunked
+    (3, 20, 128, 60, 5, "f32", 0),     # d = 128: step with 64 lanes per row
+    (5, 67, 2, 33, 6, "bf16", 0),      # d = 2: one lane per row, B not a multiple of 4
 ]
 
 
@@ -240,3 +242,34 @@ def test_chunk_plans_agree_with_oracle_on_long_prompt():
     for chunk in (0, 256, 1000, 4096, 16384):
         out = run_gpu(t, chunk_len=chunk)
         _log(f"[long] chunk={chunk} {compare_full(out, ref, w.io)}")
+
+
+def test_bf16_outputs_round_half_to_even():
+    """With lambda = 0 and R = 0 the output is h0 * u exactly in float32; with
+    h0 = 1 + 2^-8 and bfloat16 inputs every product lies exactly halfway
+    between two bfloat16 values, so the stored outputs must be the
+    ties-to-even rounding (torch's float32 -> bfloat16 conversion)."""
+    import torch
+
+    import paper_2310_18780_amd as lh
+
+    B, T, D, d = 2, 40, 96, 2
+    lam = torch.zeros((D, d), dtype=torch.complex64, device="cuda")
+    R = torch.zeros((D, d), dtype=torch.complex64, device="cuda")
+    h0 = torch.full((D,), 1.0 + 2.0 ** -8, dtype=torch.float32, device="cuda")
+    g = torch.Generator().manual_seed(0)
+    # bfloat16 values with random exponents and mantissas (odd and even)
+    u = (torch.randn((B, T, D), generator=g) * 4.0).to(torch.bfloat16)
+    ref = (u.float() * h0.cpu()).to(torch.bfloat16)
+    ud = u.cuda()
+    state = torch.empty((B, D, d), dtype=torch.complex64, device="cuda")
+    y = torch.empty_like(ud)
+    lh.prefill(lam, R, h0, ud, state, y)
+    yt = torch.empty((B, D), dtype=torch.bfloat16, device="cuda")
+    lh.step(lam, R, h0, state, ud[:, 0].contiguous(), yt)
+    torch.cuda.synchronize()
+    assert torch.equal(y.cpu().view(torch.int16), ref.view(torch.int16))
+    assert torch.equal(yt.cpu().view(torch.int16), ref[:, 0].contiguous().view(torch.int16))
+    # the ties really are ties: the float32 product is not a bfloat16 value
+    prod = u.float() * h0.cpu()
+    assert bool((prod.to(torch.bfloat16).float() != prod).float().mean() > 0.9)
