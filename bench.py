@@ -236,7 +236,10 @@ def main():
     dbytes = decode_bytes(w)
     dec_gbs = dbytes / (dec_launch_us * 1e-6) / 1e9
     pre_tf = prefill_flops(w) / (pre_avg * 1e-3) / 1e12
-    traffic = counter_traffic(f"decode_step_{w.name}_counters.txt", src_digest("decode.hip"))
+    traffic = counter_traffic(f"decode_step_{w.name}_counters.txt",
+                              src_digest("decode.hip", "lh_internal.hpp"))
+    traffic_pre = counter_traffic(f"prefill_{w.name}_counters.txt",
+                                  src_digest("prefill.hip", "lh_internal.hpp"))
 
     # HBM-streaming decode: the same kernel over a pool of state buffers larger
     # than the 256 MB Infinity Cache (like the layers of a model), so every
@@ -295,7 +298,7 @@ def main():
                      "kernel": "step_kernel", "bytes_per_launch": dbytes},
         "roofline_prefill": {"bound": "alu", "achieved": pre_tf, "peak": FP32_VALU_PEAK_TFLOPS,
                              "unit": "TFLOP/s", "frac": pre_tf / FP32_VALU_PEAK_TFLOPS,
-                             "traffic": None, "flops_per_launch": prefill_flops(w),
+                             "traffic": traffic_pre, "flops_per_launch": prefill_flops(w),
                              "bytes_per_launch": prefill_bytes(w),
                              "gbps": prefill_bytes(w) / (pre_avg * 1e-3) / 1e9},
         "decode_hbm_streaming": streaming,
