@@ -82,6 +82,9 @@ typedef enum lh_status {
 /* Largest supported number of modes per channel. */
 #define LH_MAX_MODES 1024
 
+/* chunk_len value that requests the matrix-core prefill plan (see lh_prefill). */
+#define LH_PREFILL_MFMA (-1)
+
 /* LH_ABI_VERSION of the built library. */
 int lh_abi_version(void);
 
@@ -94,7 +97,7 @@ const char* lh_last_error(void);
 
 /*
  * Workspace bytes lh_prefill needs for these sizes and chunk length
- * (chunk_len = 0 selects the automatic plan, as in lh_prefill).  Returns 0
+ * (chunk_len as in lh_prefill).  Returns 0
  * when the plan needs no workspace and (size_t)-1 when the arguments are
  * invalid.  Pure function of its arguments.
  */
@@ -111,10 +114,17 @@ size_t lh_prefill_workspace_bytes(int64_t B, int64_t D, int64_t d, int64_t T,
  *   io_dtype      : LH_F32 or LH_BF16 (u and y)
  *   state         : out, [B,D,d] complex64 (overwritten, not read)
  *   y             : out, [B,T,D] (io_dtype); may be NULL only when T == 0
- *   chunk_len     : 0 = automatic; otherwise the time-chunk length of the
- *                   chunked scan (the prompt is cut into ceil(T/chunk_len)
- *                   chunks processed in parallel; chunk_len >= T means one
- *                   sequential pass)
+ *   chunk_len     : 0 = automatic plan; > 0 = the VALU chunked scan with this
+ *                   time-chunk length (the prompt is cut into
+ *                   ceil(T/chunk_len) chunks processed in parallel; chunk_len
+ *                   >= T means one sequential pass per row);
+ *                   LH_PREFILL_MFMA = the matrix-core plan (chunks of 32
+ *                   steps as dense contractions on the MFMA units, float32
+ *                   operands split into three bfloat16 terms; requires d = 16
+ *                   or 32, D % 8 == 0, T >= 1 and 16-byte aligned u and y,
+ *                   else LH_ERR_INVALID_ARG).  The automatic plan uses the
+ *                   matrix cores where supported and the channel groups of 8
+ *                   times the 64-row batch blocks number at least 256
  *   workspace     : device scratch of at least
  *                   lh_prefill_workspace_bytes(B,D,d,T,chunk_len) bytes,
  *                   256-byte aligned; may be NULL when that size is 0.  Its

@@ -32,7 +32,10 @@ struct PrefillPlan {
     int64_t nchunks;  // ceil(T / C); 0 when T == 0
     size_t off_pow;   // workspace offset of lambda^C          [D, d] complex64
     size_t off_xin;   // workspace offset of chunk entry states [B, nchunks, D, d] complex64
-    size_t ws_bytes;  // total workspace bytes (0 when nchunks <= 1)
+    size_t ws_bytes;  // total workspace bytes (0 when nchunks <= 1 and no MFMA plan)
+    bool mfma;        // matrix-core prefill (automatic plans use it when u and y are
+                      // 16-byte aligned, else the VALU plan above)
+    bool mfma_forced; // requested explicitly: u and y must be 16-byte aligned
 };
 
 // Returns false when the sizes are invalid or overflow.
@@ -44,6 +47,15 @@ hipError_t launch_prefill(const float2* lam, const float2* R, const float* h0,
                           const void* u, bool bf16_io, int64_t B, int64_t D, int64_t d,
                           int64_t T, float2* state, void* y, const PrefillPlan& plan,
                           void* workspace, hipStream_t stream);
+
+// Matrix-core prefill (d = 16 or 32, D a multiple of 8).
+bool mfma_supported(int64_t B, int64_t D, int64_t d, int64_t T);
+bool mfma_preferred(int64_t B, int64_t D, int64_t d);
+size_t mfma_workspace_bytes(int64_t D, int64_t d);
+hipError_t launch_prefill_mfma(const float2* lam, const float2* R, const float* h0,
+                               const void* u, bool bf16_io, int64_t B, int64_t D, int64_t d,
+                               int64_t T, float2* state, void* y, void* workspace,
+                               hipStream_t stream);
 
 hipError_t launch_step(const float2* lam, const float2* R, const float* h0, float2* state,
                        const void* u_t, void* y_t, bool bf16_io, int64_t B, int64_t D,

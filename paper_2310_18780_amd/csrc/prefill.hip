@@ -290,7 +290,7 @@ inline bool grid_for(int64_t n, dim3* g)
 bool make_prefill_plan(int64_t B, int64_t D, int64_t d, int64_t T, int64_t chunk_len,
                        PrefillPlan* plan)
 {
-    if (B < 1 || D < 1 || d < 1 || d > 1024 || T < 0 || chunk_len < 0) return false;
+    if (B < 1 || D < 1 || d < 1 || d > 1024 || T < 0 || chunk_len < -1) return false;
     // element counts must fit comfortably in int64 (and the byte sizes too)
     const int64_t lim = INT64_C(1) << 58;
     if (B > lim / D || B * D > lim / (T > d ? (T > 0 ? T : 1) : d)) return false;
@@ -337,6 +337,17 @@ bool make_prefill_plan(int64_t B, int64_t D, int64_t d, int64_t T, int64_t chunk
         p.off_xin = (pow_bytes + 255) / 256 * 256;
         p.ws_bytes = p.off_xin + static_cast<size_t>(B) * p.nchunks * D * d * sizeof(float2);
     }
+    // The automatic plan runs on the matrix cores where supported; the
+    // workspace also covers the VALU plan above, taken when u or y is not
+    // 16-byte aligned.
+    p.mfma_forced = chunk_len == -1;
+    if (p.mfma_forced && !mfma_supported(B, D, d, T)) return false;
+    p.mfma = p.mfma_forced ||
+             (chunk_len == 0 && mfma_supported(B, D, d, T) && mfma_preferred(B, D, d));
+    if (p.mfma) {
+        const size_t mb = mfma_workspace_bytes(D, d);
+        if (p.mfma_forced || mb > p.ws_bytes) p.ws_bytes = mb;  // a forced plan has no fallback
+    }
     *plan = p;
     return true;
 }
@@ -354,6 +365,11 @@ hipError_t launch_prefill(const float2* lam, const float2* R, const float* h0, c
         hipLaunchKernelGGL(zero_kernel, g_state, dim3(kBlock), 0, stream, state, B * D * d);
         return hipGetLastError();
     }
+    const bool aligned16 = reinterpret_cast<uintptr_t>(u) % 16 == 0 &&
+                           reinterpret_cast<uintptr_t>(y) % 16 == 0;
+    if (p.mfma && aligned16)
+        return launch_prefill_mfma(lam, R, h0, u, bf16_io, B, D, d, T, state, y, workspace,
+                                   stream);
     float2* lamC = nullptr;
     float2* xs = nullptr;
     hipError_t e;

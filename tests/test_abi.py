@@ -74,10 +74,23 @@ def test_workspace_sizes():
     nch = -(-T // C)
     pow_bytes = -(-(D * d * 8) // 256) * 256
     assert lh.workspace_bytes(B, D, d, T, chunk_len=C) == pow_bytes + B * nch * D * d * 8
-    # automatic plan of the long-prompt workload is chunked, of the wide ones not
-    assert lh.workspace_bytes(4, 1024, 32, 65536) > 0
-    assert lh.workspace_bytes(64, 2048, 16, 4096) == 0
+    # automatic plans: matrix-core tables for d = 16 / 32 with D % 8 == 0
+    # (bfloat16 fragments of P, T, W: (4 d/16 + 2) x 3 x 64 x 16 B per channel, plus
+    # lambda^C), the VALU plan otherwise (one pass for the wide d = 64 workload)
+    frag = lambda D, d: D * (4 * (d // 16) + 2) * 3 * 64 * 16  # noqa: E731
+    assert lh.workspace_bytes(64, 2048, 16, 4096) == -(-frag(2048, 16) // 256) * 256 + 2048 * 16 * 8
+    # the explicit matrix-core plan needs the same tables
+    assert lh.workspace_bytes(4, 1024, 32, 65536, chunk_len=-1) == frag(1024, 32) + 1024 * 32 * 8
+    # long prompt, few rows: the automatic plan keeps the VALU chunked scan
+    # (32 chunks of 2048 steps) for its parallelism along time
+    assert lh.workspace_bytes(4, 1024, 32, 65536) == 1024 * 32 * 8 + 4 * 32 * 1024 * 32 * 8
+    # the matrix-core plan needs d = 16 / 32 and D % 8 == 0
+    bad = ctypes.c_size_t(-1).value
+    assert lh.lib().lh_prefill_workspace_bytes(2, 12, 16, 64, -1) == bad
+    assert lh.lib().lh_prefill_workspace_bytes(2, 16, 64, 64, -1) == bad
     assert lh.workspace_bytes(256, 2048, 64, 1024) == 0
+    # D % 8 != 0: VALU plan, few rows -> 5 chunks of 64 steps
+    assert lh.workspace_bytes(2, 70, 16, 300) == 70 * 16 * 8 + 2 * 5 * 70 * 16 * 8
     # invalid sizes
     L = lh.lib()
     bad = ctypes.c_size_t(-1).value

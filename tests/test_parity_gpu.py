@@ -68,6 +68,19 @@ SMALL = [
     (1, 8, 4, 40, 3, "f32", 39),       # two chunks, last of length 1
     (4, 256, 16, 512, 8, "bf16", 64),  # many waves, bf16, chunked
     (3, 20, 128, 60, 5, "f32", 0),     # d = 128: step with 64 lanes per row
+    # matrix-core prefill (chunk_len = -1 = LH_PREFILL_MFMA; d = 16 / 32, D % 8 == 0)
+    (2, 64, 16, 300, 20, "f32", -1),   # ragged last chunk (300 = 9*32 + 12), 14 idle columns
+    (3, 136, 16, 257, 9, "bf16", -1),  # 17 channel groups (partial line group), 257 = 8*32 + 1
+    (17, 16, 32, 100, 5, "f32", -1),   # d = 32, second batch block of one row
+    (1, 8, 32, 31, 3, "bf16", -1),     # T < 32: one partial chunk
+    (2, 8, 16, 32, 2, "f32", -1),      # exactly one full chunk
+    (2, 8, 16, 64, 2, "bf16", -1),     # two full chunks
+    (1, 8, 16, 1, 3, "f32", -1),       # T = 1
+    (4, 256, 16, 512, 8, "bf16", -1),  # many workgroups
+    (33, 72, 32, 160, 4, "f32", -1),   # three batch blocks, 9 channel groups
+    (70, 24, 16, 97, 3, "bf16", -1),   # 4 batch groups per workgroup, 2 blocks, 6 rows in the last
+    (40, 16, 16, 200, 3, "f32", -1),   # 2 batch groups per workgroup (float32), ragged
+    (20, 8, 16, 65, 2, "bf16", -1),    # 2 batch groups per workgroup (bfloat16)
     (5, 67, 2, 33, 6, "bf16", 0),      # d = 2: one lane per row, B not a multiple of 4
 ]
 
