@@ -239,7 +239,7 @@ def main():
     traffic = counter_traffic(f"decode_step_{w.name}_counters.txt",
                               src_digest("decode.hip", "lh_internal.hpp"))
     traffic_pre = counter_traffic(f"prefill_{w.name}_counters.txt",
-                                  src_digest("prefill.hip", "lh_internal.hpp"))
+                                  src_digest("prefill.hip", "prefill_mfma.hip", "lh_internal.hpp"))
 
     # HBM-streaming decode: the same kernel over a pool of state buffers larger
     # than the 256 MB Infinity Cache (like the layers of a model), so every

@@ -14,7 +14,10 @@
 // the state; the row sum is a butterfly over those lanes.  Each thread serves
 // NB = 4 batch rows of the same (c, mode pair): lambda and R are loaded once
 // for the four rows, and every thread has four independent 16-byte state loads
-// in flight before it computes.  Two memory policies, chosen by state size:
+// in flight before it computes.  Outputs y_t are stored non-temporally (written
+// once, read by the next layer, not by this kernel), so that they do not
+// displace the state from the caches.  Two memory policies, chosen by state
+// size:
 //
 //  * resident (state < 128 MiB, can stay in the 256 MB Infinity Cache between
 //    steps): ordinary loads, non-temporal stores, consecutive workgroups on the
@@ -117,7 +120,7 @@ __global__ __launch_bounds__(kBlock) void step_pairs_kernel(
         if (cvalid && b < B) {
             const int64_t row = int64_t(b) * D + c;
             store4(state + row * d + 2 * j, n4, true);
-            if (j == 0) io_store(y + row, fmaf(hz, uv[i], acc));
+            if (j == 0) io_store_nt(y + row, fmaf(hz, uv[i], acc));
         }
     }
 }

@@ -24,6 +24,13 @@ __device__ __forceinline__ void io_store(bf16* p, float v) {
     p->bits = __builtin_bit_cast(uint16_t, static_cast<__bf16>(v));
 }
 
+// Non-temporal variants (written once, not re-read soon): keep the cache for
+// data that is.
+__device__ __forceinline__ void io_store_nt(float* p, float v) { __builtin_nontemporal_store(v, p); }
+__device__ __forceinline__ void io_store_nt(bf16* p, float v) {
+    __builtin_nontemporal_store(__builtin_bit_cast(uint16_t, static_cast<__bf16>(v)), &p->bits);
+}
+
 // How the prefill of one call is cut up.
 struct PrefillPlan {
     int lpr;          // lanes per (b, c) row: the modes of a row are split over lpr lanes
