@@ -11,7 +11,7 @@
 // Fast path (d even, d/2 a power of two <= 128, 16-byte aligned arrays): the
 // d/2 mode pairs of a (b, c) row sit on LPR = d/2 consecutive lanes, one
 // 16-byte access each, so a wavefront reads and writes one contiguous span of
-// the state; the row sum is a butterfly over those lanes.  Each thread serves
+// the state; the row sum is a butterfly over those lanes (DPP within 16 lanes).  Each thread serves
 // NB = 4 batch rows of the same (c, mode pair): lambda and R are loaded once
 // for the four rows, and every thread has four independent 16-byte state loads
 // in flight before it computes.  Outputs y_t are stored non-temporally (written
@@ -56,6 +56,41 @@ __device__ __forceinline__ void store4(float2* p, float4 a, bool nt)
         __builtin_nontemporal_store(v, q);
     else
         *q = v;
+}
+
+// Butterfly step of a row sum over LPR lanes: after the steps for offsets
+// 1 .. off/2 every aligned group of `off` lanes holds one partial sum, so any
+// lane permutation that pairs each group with its neighbour group completes
+// the step.  Within a row of 16 lanes this is DPP on the VALU (quad_perm for
+// 1 and 2, half-row mirror for 4, row mirror for 8); wider steps use a shuffle.
+template <int OFF>
+__device__ __forceinline__ float butterfly(float v)
+{
+    const int x = __builtin_bit_cast(int, v);
+    int p;
+    if constexpr (OFF == 1)
+        p = __builtin_amdgcn_mov_dpp(x, 0xB1, 0xF, 0xF, false);   // quad_perm [1,0,3,2]
+    else if constexpr (OFF == 2)
+        p = __builtin_amdgcn_mov_dpp(x, 0x4E, 0xF, 0xF, false);   // quad_perm [2,3,0,1]
+    else if constexpr (OFF == 4)
+        p = __builtin_amdgcn_mov_dpp(x, 0x141, 0xF, 0xF, false);  // row_half_mirror
+    else if constexpr (OFF == 8)
+        p = __builtin_amdgcn_mov_dpp(x, 0x140, 0xF, 0xF, false);  // row_mirror
+    else
+        return v + __shfl_xor(v, OFF, 64);
+    return v + __builtin_bit_cast(float, p);
+}
+
+template <int LPR>
+__device__ __forceinline__ float row_sum(float v)
+{
+    if constexpr (LPR >= 2) v = butterfly<1>(v);
+    if constexpr (LPR >= 4) v = butterfly<2>(v);
+    if constexpr (LPR >= 8) v = butterfly<4>(v);
+    if constexpr (LPR >= 16) v = butterfly<8>(v);
+    if constexpr (LPR >= 32) v = butterfly<16>(v);
+    if constexpr (LPR >= 64) v = butterfly<32>(v);
+    return v;
 }
 
 // complex multiply-add of two modes held as (re0, im0, re1, im1)
@@ -113,10 +148,8 @@ __global__ __launch_bounds__(kBlock) void step_pairs_kernel(
 #pragma unroll
     for (int i = 0; i < NB; ++i) {
         const int b = b0 + i;
-        float acc = re_dot_pair(r4, x[i]);
+        const float acc = row_sum<LPR>(re_dot_pair(r4, x[i]));
         const float4 n4 = step_pair(l4, x[i], uv[i]);
-#pragma unroll
-        for (int off = 1; off < LPR; off <<= 1) acc += __shfl_xor(acc, off, LPR);
         if (cvalid && b < B) {
             const int64_t row = int64_t(b) * D + c;
             store4(state + row * d + 2 * j, n4, true);
@@ -170,8 +203,7 @@ __global__ __launch_bounds__(kBlock) void step_generic_kernel(
             if (valid) xrow[m] = n2;
         }
     }
-#pragma unroll
-    for (int off = 1; off < LPR; off <<= 1) acc += __shfl_xor(acc, off, LPR);
+    acc = row_sum<LPR>(acc);
     if (valid && j == 0) io_store(y + b * D + c, fmaf(h0[c], uv, acc));
 }
 
