@@ -8,24 +8,22 @@
 // kernel is bound by memory bandwidth (16 bytes of state traffic per mode
 // against 12 flops).
 //
-// Fast path (d even, d/2 a power of two <= 128, 16-byte aligned arrays): the
+// Fast path (d even, d/2 a power of two <= 64, 16-byte aligned arrays): the
 // d/2 mode pairs of a (b, c) row sit on LPR = d/2 consecutive lanes, one
-// 16-byte access each, so a wavefront reads and writes one contiguous span of
-// the state; the row sum is a butterfly over those lanes (DPP within 16 lanes).  Each thread serves
-// NB = 4 batch rows of the same (c, mode pair): lambda and R are loaded once
-// for the four rows, and every thread has four independent 16-byte state loads
-// in flight before it computes.  Outputs y_t are stored non-temporally (written
-// once, read by the next layer, not by this kernel), so that they do not
-// displace the state from the caches.  Two memory policies, chosen by state
-// size:
-//
-//  * resident (state < 128 MiB, can stay in the 256 MB Infinity Cache between
-//    steps): ordinary loads, non-temporal stores, consecutive workgroups on the
-//    same channel tile;
-//  * streaming (larger states): non-temporal loads and stores, consecutive
-//    workgroups on consecutive channel tiles with the tile count padded to a
-//    multiple of 8, so that (workgroup i runs on XCD i mod 8) every channel
-//    tile and its lambda/R stay on one XCD.
+// 16-byte access each, so a wavefront reads and writes one contiguous span
+// of the state; the row sum is a butterfly over those lanes (DPP within 16
+// lanes).  Each thread serves NB = 4 batch rows of the same (c, mode pair):
+// lambda and R are loaded once for the four rows, and every thread has four
+// independent 16-byte state loads in flight before it computes.  State loads
+// are ordinary; state stores and the outputs y_t are non-temporal (written
+// once, not re-read by this kernel). Workgroups are ordered channel tile
+// fastest, with the tile count padded to a multiple of 8: workgroup i runs
+// on XCD i mod 8, so every channel tile (its lambda/R and its slice of the
+// state) is served by one XCD's L2 for all batch groups.  Measured against
+// the batch-group-fastest order, this order is faster whenever the state or
+// u_t comes from HBM rather than the Infinity Cache (inputs u_t prepared
+// long before the step, or a model whose layer states together exceed the
+// 256 MB cache); it is slower only when all operands are already cached.
 //
 // Generic path (any other d): lanes take single modes j, j + LPR, ...
 // (LPR = next power of two >= d, <= 64) or pairs, one batch row per thread.
@@ -37,22 +35,31 @@ namespace {
 constexpr int kBlock = 256;
 constexpr int kXcds = 8;
 constexpr int kRowsPerThread = 4;
-constexpr int64_t kResidentStateBytes = int64_t(128) << 20;
 
 typedef float f4v __attribute__((ext_vector_type(4)));
 
-__device__ __forceinline__ float4 load4(const float2* p, bool nt)
+// 16-byte accesses.  NT is a template argument, not a run-time flag: with a
+// flag, both branches would store the same value to the same address and the
+// compiler merges them into one plain access before the flag is known,
+// dropping the non-temporal hint.
+template <bool NT>
+__device__ __forceinline__ float4 load4(const float2* p)
 {
     const f4v* q = reinterpret_cast<const f4v*>(p);
-    const f4v v = nt ? __builtin_nontemporal_load(q) : *q;
+    f4v v;
+    if constexpr (NT)
+        v = __builtin_nontemporal_load(q);
+    else
+        v = *q;
     return make_float4(v.x, v.y, v.z, v.w);
 }
 
-__device__ __forceinline__ void store4(float2* p, float4 a, bool nt)
+template <bool NT>
+__device__ __forceinline__ void store4(float2* p, float4 a)
 {
     f4v* q = reinterpret_cast<f4v*>(p);
     const f4v v = {a.x, a.y, a.z, a.w};
-    if (nt)
+    if constexpr (NT)
         __builtin_nontemporal_store(v, q);
     else
         *q = v;
@@ -110,13 +117,9 @@ __device__ __forceinline__ float re_dot_pair(float4 r, float4 x)
 }
 
 // Fast path: LPR = d / 2 lanes per row, NB rows per thread, 2-D grid of
-// (channel tile, batch group) blocks, so no integer division is needed to
-// place a block.  Resident policy: blockIdx.x = batch group (consecutive
-// blocks share a channel tile), plain loads, non-temporal stores.  Streaming
-// policy: blockIdx.x = channel tile with gridDim.x a multiple of 8, so each
-// channel tile (and its lambda/R) lives on one XCD for all batch groups;
-// non-temporal loads and stores.
-template <typename IO, int LPR, bool STREAM>
+// (channel tile, batch group) blocks, blockIdx.x = channel tile with gridDim.x
+// a multiple of 8, so no integer division is needed to place a block.
+template <typename IO, int LPR>
 __global__ __launch_bounds__(kBlock) void step_pairs_kernel(
     const float2* __restrict__ lam, const float2* __restrict__ R, const float* __restrict__ h0,
     float2* __restrict__ state, const IO* __restrict__ u, IO* __restrict__ y, int B, int D,
@@ -125,23 +128,23 @@ __global__ __launch_bounds__(kBlock) void step_pairs_kernel(
     constexpr int NB = kRowsPerThread;
     constexpr int kRows = kBlock / LPR;  // channels per block
     constexpr int d = 2 * LPR;
-    const int ct = STREAM ? blockIdx.x : blockIdx.y;  // channel tile
-    const int b0 = (STREAM ? blockIdx.y : blockIdx.x) * NB;
-    if (ct >= ntiles) return;  // padding tiles of the streaming grid
+    const int ct = blockIdx.x;  // channel tile
+    const int b0 = blockIdx.y * NB;
+    if (ct >= ntiles) return;  // padding tiles
     const int j = threadIdx.x % LPR;
     const int c = ct * kRows + threadIdx.x / LPR;
     const bool cvalid = c < D;
     const int cc = cvalid ? c : D - 1;  // every address stays in bounds
 
-    const float4 l4 = load4(lam + int64_t(cc) * d + 2 * j, false);
-    const float4 r4 = load4(R + int64_t(cc) * d + 2 * j, false);
+    const float4 l4 = load4<false>(lam + int64_t(cc) * d + 2 * j);
+    const float4 r4 = load4<false>(R + int64_t(cc) * d + 2 * j);
     float4 x[NB];
     float uv[NB];
 #pragma unroll
     for (int i = 0; i < NB; ++i) {
         const int b = (b0 + i < B) ? b0 + i : B - 1;
         const int64_t row = int64_t(b) * D + cc;
-        x[i] = load4(state + row * d + 2 * j, STREAM);
+        x[i] = load4<false>(state + row * d + 2 * j);
         uv[i] = io_load(u + row);
     }
     const float hz = h0[cc];
@@ -152,7 +155,7 @@ __global__ __launch_bounds__(kBlock) void step_pairs_kernel(
         const float4 n4 = step_pair(l4, x[i], uv[i]);
         if (cvalid && b < B) {
             const int64_t row = int64_t(b) * D + c;
-            store4(state + row * d + 2 * j, n4, true);
+            store4<true>(state + row * d + 2 * j, n4);
             if (j == 0) io_store_nt(y + row, fmaf(hz, uv[i], acc));
         }
     }
@@ -185,10 +188,10 @@ __global__ __launch_bounds__(kBlock) void step_generic_kernel(
         const int64_t ni = d / (2 * LPR);
         for (int64_t i = 0; i < ni; ++i) {
             const int64_t m = 2 * (j + i * LPR);
-            const float4 x4 = load4(xrow + m, false);
-            acc += re_dot_pair(load4(rrow + m, false), x4);
-            const float4 n4 = step_pair(load4(lrow + m, false), x4, uv);
-            if (valid) store4(xrow + m, n4, false);
+            const float4 x4 = load4<false>(xrow + m);
+            acc += re_dot_pair(load4<false>(rrow + m), x4);
+            const float4 n4 = step_pair(load4<false>(lrow + m), x4, uv);
+            if (valid) store4<false>(xrow + m, n4);
         }
     } else {
         for (int64_t m = j; m < d; m += LPR) {
@@ -208,39 +211,30 @@ __global__ __launch_bounds__(kBlock) void step_generic_kernel(
 }
 
 // 2-D grid of the fast path; false when it does not fit the grid limits
-bool pairs_grid(int lpr, bool stream_policy, int64_t B, int64_t D, dim3* g, int* ntiles)
+bool pairs_grid(int lpr, int64_t B, int64_t D, dim3* g, int* ntiles)
 {
     const int64_t rows_per_block = kBlock / lpr;
     const int64_t nt = (D + rows_per_block - 1) / rows_per_block;
     const int64_t nbg = (B + kRowsPerThread - 1) / kRowsPerThread;
     const int64_t ntp = (nt + kXcds - 1) / kXcds * kXcds;
-    if (stream_policy) {
-        if (ntp > 0x7fffffff || nbg > 65535) return false;
-        *g = dim3(uint32_t(ntp), uint32_t(nbg));
-    } else {
-        if (nbg > 0x7fffffff || nt > 65535) return false;
-        *g = dim3(uint32_t(nbg), uint32_t(nt));
-    }
+    if (ntp > 0x7fffffff || nbg > 65535) return false;
+    *g = dim3(uint32_t(ntp), uint32_t(nbg));
     *ntiles = int(nt);
     return true;
 }
 
 template <typename IO>
-hipError_t launch_pairs(int lpr, bool stream_policy, dim3 grid, int ntiles, const float2* lam,
-                        const float2* R, const float* h0, float2* state, const void* u, void* y,
-                        int64_t B, int64_t D, hipStream_t stream)
+hipError_t launch_pairs(int lpr, dim3 grid, int ntiles, const float2* lam, const float2* R,
+                        const float* h0, float2* state, const void* u, void* y, int64_t B,
+                        int64_t D, hipStream_t stream)
 {
     const IO* uu = static_cast<const IO*>(u);
     IO* yy = static_cast<IO*>(y);
     const int b = int(B), dd = int(D);
-#define LH_PAIRS(L)                                                                            \
-    case L:                                                                                    \
-        if (stream_policy)                                                                     \
-            hipLaunchKernelGGL((step_pairs_kernel<IO, L, true>), grid, dim3(kBlock), 0, stream, \
-                               lam, R, h0, state, uu, yy, b, dd, ntiles);                      \
-        else                                                                                   \
-            hipLaunchKernelGGL((step_pairs_kernel<IO, L, false>), grid, dim3(kBlock), 0,       \
-                               stream, lam, R, h0, state, uu, yy, b, dd, ntiles);              \
+#define LH_PAIRS(L)                                                                          \
+    case L:                                                                                  \
+        hipLaunchKernelGGL((step_pairs_kernel<IO, L>), grid, dim3(kBlock), 0, stream, lam, R, \
+                           h0, state, uu, yy, b, dd, ntiles);                                \
         break;
     switch (lpr) {
         LH_PAIRS(1)
@@ -299,14 +293,13 @@ hipError_t launch_step(const float2* lam, const float2* R, const float* h0, floa
     const bool pow2_pairs = d % 2 == 0 && pairs >= 1 && pairs <= 64 && (pairs & (pairs - 1)) == 0;
     dim3 grid;
     int ntiles = 0;
-    const bool stream_policy = 8 * B * D * d >= kResidentStateBytes;
     const int fast_lpr = static_cast<int>(pairs);
     if (pow2_pairs && aligned16 && B < (INT64_C(1) << 31) && D < (INT64_C(1) << 31) &&
-        pairs_grid(fast_lpr, stream_policy, B, D, &grid, &ntiles)) {
-        return bf16_io ? launch_pairs<bf16>(fast_lpr, stream_policy, grid, ntiles, lam, R, h0,
-                                            state, u_t, y_t, B, D, stream)
-                       : launch_pairs<float>(fast_lpr, stream_policy, grid, ntiles, lam, R, h0,
-                                             state, u_t, y_t, B, D, stream);
+        pairs_grid(fast_lpr, B, D, &grid, &ntiles)) {
+        return bf16_io ? launch_pairs<bf16>(fast_lpr, grid, ntiles, lam, R, h0, state, u_t, y_t,
+                                            B, D, stream)
+                       : launch_pairs<float>(fast_lpr, grid, ntiles, lam, R, h0, state, u_t,
+                                             y_t, B, D, stream);
     }
     // generic layouts
     int lpr = 1;
