@@ -120,11 +120,13 @@ size_t lh_prefill_workspace_bytes(int64_t B, int64_t D, int64_t d, int64_t T,
  *                   >= T means one sequential pass per row);
  *                   LH_PREFILL_MFMA = the matrix-core plan (chunks of 32
  *                   steps as dense contractions on the MFMA units, float32
- *                   operands split into three bfloat16 terms; requires d = 16
- *                   or 32, D % 8 == 0, T >= 1 and 16-byte aligned u and y,
- *                   else LH_ERR_INVALID_ARG).  The automatic plan uses the
- *                   matrix cores where supported and the channel groups of 8
- *                   times the 64-row batch blocks number at least 256
+ *                   operands split into bfloat16 terms: three with float32
+ *                   u/y, two with bfloat16 u/y; requires d = 16 or 32,
+ *                   D % 8 == 0, T >= 1 and 16-byte aligned u and y, else
+ *                   LH_ERR_INVALID_ARG).  The automatic plan uses the matrix
+ *                   cores where supported and ceil(D/16) * ceil(B/32) >= 256
+ *                   (enough workgroups to fill the GPU without splitting the
+ *                   prompt in time)
  *   workspace     : device scratch of at least
  *                   lh_prefill_workspace_bytes(B,D,d,T,chunk_len) bytes,
  *                   256-byte aligned; may be NULL when that size is 0.  Its

@@ -18,30 +18,35 @@
 //
 // so that y_t = Re(R x_t) + h0 u_t at every step and the last carry is x_T.
 //
-// Arithmetic: v_mfma_f32_16x16x32_bf16 (float32 accumulation).  Every float32
-// operand is split into three bfloat16 terms a = a1 + a2 + a3 (each the
-// nearest bfloat16 of what the previous terms leave: 24 significant bits) and
-// a product a b is accumulated as the six terms ai bj with i + j <= 4, which
-// leaves an error of a few float32 ulps of |a b|; bfloat16 inputs are exact in
-// one term, so their products take three MFMAs.  The carried state enters the
-// output correction W X_in in two terms (four products; relative error near
-// 2^-16 in that correction only, the carry itself stays float32).  The per-channel matrices and
-// lambda^C come from float64 powers, rounded once to float32 and split by the
-// setup kernel into the workspace, already in the lane order of the A operand.
+// Arithmetic: v_mfma_f32_16x16x32_bf16 (float32 accumulation).  A float32
+// operand is split into bfloat16 terms a = a1 + a2 (+ a3), each the nearest
+// bfloat16 of what the previous terms leave, and a product a b is accumulated
+// as the terms ai bj with i + j below the term count.  With float32 inputs
+// every operand takes three terms (24 significant bits; six products, an
+// error of a few float32 ulps of |a b|).  Bfloat16 inputs are exact in one
+// term and their outputs are rounded to bfloat16, so the matrices take two
+// terms (relative error near 2^-17, far below the output rounding and the
+// float32 state tolerance) and each product two MFMAs.  The carried state
+// enters the output correction W X_in in two terms (relative error near 2^-16
+// in that correction only; the carry itself stays float32).  The per-channel
+// matrices and lambda^C come from float64 powers, rounded once to float32 and
+// split by the setup kernel into the workspace, already in the lane order of
+// the A operand.
 //
-// Work layout: a wavefront owns one channel and NBG groups of 16 batch rows
-// and walks all chunks of the prompt, keeping its matrices (A operands) and
-// the carried states in registers.  With the 16x16 accumulator layout (lane
-// n + 16 g holds rows 4g..4g+3 of column n) and state rows ordered
-// [Re modes | Im modes], the real and imaginary parts of a mode sit in the
-// same lane, so the carry is lane-local, and X_in itself is the B operand of
-// W X_in once W's columns are permuted to match (K index 8g + i <-> the
-// lane's rows).  A workgroup is 8 waves = 8 consecutive channels.  The u tile
-// of a chunk is staged through LDS (transposed to [channel][row][step]) from
-// registers loaded one chunk ahead; the outputs go back through LDS so that
-// every global access covers 8 channels.  Barriers order LDS only, so the
-// prefetch stays in flight across them.
-// Workgroups are ordered so that the 8 channel groups sharing 128-byte lines
+// Work layout: a wavefront owns CPW channels (2 for bfloat16 inputs with
+// d = 16, else 1) and NBG groups of 16 batch rows, and walks all chunks of the
+// prompt, keeping its matrices (A operands) and the carried states in
+// registers.  With the 16x16 accumulator layout (lane n + 16 g holds rows
+// 4g..4g+3 of column n) and state rows ordered [Re modes | Im modes], the
+// real and imaginary parts of a mode sit in the same lane, so the carry is
+// lane-local, and X_in itself is the B operand of W X_in once W's columns are
+// permuted to match (K index 8g + i <-> the lane's rows).  A workgroup is 8
+// waves = 8 CPW consecutive channels.  The u tile of a chunk is staged
+// through LDS (transposed to [channel][row][step]) from registers loaded one
+// chunk ahead; the outputs go back through LDS so that every global access is
+// a 16-byte piece of a whole (row, step) segment of the workgroup's channels.
+// Barriers order LDS only, so the prefetch stays in flight across them.
+// Workgroups are ordered so that the channel groups sharing 128-byte lines
 // of u and y run on one XCD (workgroup i runs on XCD i mod 8).
 //
 // A last chunk shorter than C is computed with zero-padded inputs (causality
@@ -57,10 +62,7 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kC = 32;     // chunk length = K of the MFMA
 constexpr int kN = 16;     // batch rows per MFMA column block
-constexpr int kW = 8;      // waves (channels) per workgroup
-constexpr int kThreads = 64 * kW;
 constexpr int kTerms = 3;  // bfloat16 terms of a split float32
-constexpr int kYPad = 2;   // LDS padding (elements) of an output-stage row
 constexpr int kMinWorkgroups = 256;  // automatic plan: at least one workgroup per CU
 
 // A-operand fragments per channel: P (2d/16 tiles), T (2 tiles), W (2 tiles x d/16 K-steps)
@@ -180,159 +182,205 @@ __global__ __launch_bounds__(256) void mfma_setup_kernel(const float2* __restric
 }
 
 // ------------------------------------------------------------- main kernel
-// LDS element type of the staged u tile: bfloat16 inputs as they are, float32
-// inputs as float32 (split into terms when read as the B operand).
+// Tiling per (IO, DM): a wave owns CPW channels and NBG groups of 16 batch
+// rows; a workgroup of 8 waves owns CW = 8 CPW consecutive channels, so that
+// one (row, step) of its inputs or outputs is a CW-channel segment of a
+// 128-byte line.  Lines of u and y are shared by the workgroups of
+// neighbouring channel groups, and the partial-line traffic, not the
+// arithmetic, bounds the kernel: two channels per wave (32-byte segments for
+// bfloat16) cut it by about a sixth against one (16-byte segments).  A wider
+// segment would need the A operands of more channels than the register file
+// holds next to the carried states.
+template <typename IO, int DM>
+struct Tiling;
+template <>
+struct Tiling<bf16, 1> {
+    static constexpr int CPW = 2;
+};
+template <>
+struct Tiling<bf16, 2> {
+    static constexpr int CPW = 1;
+};
+template <>
+struct Tiling<float, 1> {
+    static constexpr int CPW = 1;
+};
+template <>
+struct Tiling<float, 2> {
+    static constexpr int CPW = 1;
+};
+constexpr int kW = 8;  // waves per workgroup
+constexpr int kThreads = 64 * kW;
+
+// LDS element type of the staged u tile and operand term counts: bfloat16
+// inputs are exact in one term and their outputs are rounded to bfloat16, so
+// two-term A operands (relative error near 2^-17) suffice; float32 inputs and
+// A operands take three terms.
 template <typename IO>
 struct Stage;
 template <>
 struct Stage<bf16> {
     typedef __bf16 T;
     static constexpr int kNTU = 1;
+    static constexpr int kNTA = 2;
 };
 template <>
 struct Stage<float> {
     typedef float T;
     static constexpr int kNTU = kTerms;
+    static constexpr int kNTA = kTerms;
 };
 
 template <typename IO, int DM, int NBG>
 __global__ __launch_bounds__(kThreads) void mfma_prefill_kernel(
     const float2* __restrict__ lam, const IO* __restrict__ u, IO* __restrict__ y,
     float2* __restrict__ state, const bf16x8* __restrict__ frag,
-    const float2* __restrict__ lamc, int B, int D, int64_t T, int ncg, int nbg, int nlg,
-    int per_xcd)
+    const float2* __restrict__ lamc, int B, int D, int64_t T, int ncg, int nbg, int per_xcd)
 {
     constexpr int d = 16 * DM;
     constexpr int F = n_frag(DM);
+    constexpr int CPW = Tiling<IO, DM>::CPW;
+    constexpr int CW = kW * CPW;
     constexpr int BN = kN * NBG;                      // batch rows per workgroup
     constexpr int NTU = Stage<IO>::kNTU;
+    constexpr int KT = Stage<IO>::kNTA;
     typedef typename Stage<IO>::T ST;
-    constexpr int kRowBytes = kW * int(sizeof(IO));   // one (row, step) of 8 channels
-    constexpr int kRaw = kRowBytes / 16;              // 16-byte loads per (row, step)
-    constexpr int kPairs = BN * kC / 2;               // (row, step pair) items per chunk
-    constexpr int kPPT = (kPairs + kThreads - 1) / kThreads;  // items per thread
-    constexpr int kYRow = kC * kW + kYPad;            // IO elements per output-stage row
-    __shared__ __attribute__((aligned(16))) ST ubuf[1][kW * BN * kC];
-    __shared__ __attribute__((aligned(16))) IO ystage[BN * kYRow];
+    constexpr int ES = int(sizeof(IO));
+    constexpr int CPP = 16 / ES;                      // channels per 16-byte piece
+    constexpr int PPR = CW / CPP;                     // pieces per (row, step)
+    constexpr int NITEM = BN * (kC / 2) * PPR;        // (row, step pair, piece) items
+    constexpr int IPT = (NITEM + kThreads - 1) / kThreads;  // items per thread
+    constexpr int US = kC + 16 / int(sizeof(ST));     // u stage: steps per (channel, row), padded
+    // y stage in 32-bit words: (row, step) cells of SD words, rows padded to
+    // 4 words past a multiple of 32 and the words of each 16-byte piece
+    // permuted by (step >> 2) & 3 (see ysw), so that a wave's stores (16 rows x
+    // 4 lane groups, one word each) fall on every LDS bank exactly twice
+    constexpr int SD = CW * ES / 4;                   // words per (row, step)
+    constexpr int RS = kC * SD + 4;                   // words per row
+    constexpr int NYP = BN * kC * PPR;                // 16-byte output pieces per chunk
+    __shared__ __attribute__((aligned(16))) ST ubuf[CW * BN * US];
+    __shared__ __attribute__((aligned(16))) uint32_t ystage[BN * RS];
+    __shared__ __attribute__((aligned(16))) float2 lcs[CW][4][4 * DM];  // lambda^C per channel, lane group
 
-    // ---- workgroup -> (channel group, batch group), XCD-aware
+    // ---- workgroup -> (channel group, batch group); logical index lin runs
+    // on XCD lin / per_xcd (workgroup i runs on XCD i mod 8), so consecutive
+    // channel groups, which share the 128-byte lines of u and y, meet in one L2
     const int hw = blockIdx.x;
     const int lin = (hw % 8) * per_xcd + hw / 8;
-    const int rest = lin / 8;
-    const int cg = (rest % nlg) * 8 + lin % 8;
-    const int bgw = rest / nlg;
-    if (bgw >= nbg || cg >= ncg) return;  // whole workgroup exits together
-    const int c0 = cg * kW;
+    const int cg = lin % ncg;
+    const int bgw = lin / ncg;
+    if (bgw >= nbg) return;  // whole workgroup exits together
+    const int c0 = cg * CW;
     const int b0 = bgw * BN;
 
     const int tid = threadIdx.x;
     const int w = tid / 64, lane = tid % 64;
     const int g = lane / 16, n = lane % 16;
-    const int c = c0 + w;  // this wave's channel (D % 8 == 0, so c < D)
 
-    // ---- A operands and lambda^C into registers
-    bf16x8 A[F][kTerms];
+    // ---- A operands and lambda^C of this wave's channels (clamped into range;
+    // results of channels >= D are never stored)
+    bf16x8 A[CPW][F][KT];
 #pragma unroll
-    for (int f = 0; f < F; ++f)
+    for (int k = 0; k < CPW; ++k) {
+        const int cc = min(c0 + w * CPW + k, D - 1);
 #pragma unroll
-        for (int s = 0; s < kTerms; ++s)
-            A[f][s] = frag[((int64_t(c) * F + f) * kTerms + s) * 64 + lane];
-    float lcr[DM][4], lci[DM][4];
+        for (int f = 0; f < F; ++f)
 #pragma unroll
-    for (int q = 0; q < DM; ++q)
+            for (int s = 0; s < KT; ++s)
+                A[k][f][s] = frag[((int64_t(cc) * F + f) * kTerms + s) * 64 + lane];
+        if (n < 4 * DM)  // lambda^C of the modes of lane group g (read back by the carry)
+            lcs[w * CPW + k][g][n] = lamc[(int64_t(cc) * 4 + g) * (4 * DM) + n];
+    }
+    // carried states: X[k][bg][mt][i] = row 16 mt + 4 g + i of column n of
+    // batch group bg; tiles q < DM hold Re of modes 16 q + 4 g + i, tiles
+    // DM + q their Im
+    f32x4 X[CPW][NBG][2 * DM];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const float2 v = lamc[(int64_t(c) * 4 + g) * (4 * DM) + q * 4 + i];
-            lcr[q][i] = v.x;
-            lci[q][i] = v.y;
-        }
-    // carried states: X[bg][mt][i] = row 16 mt + 4 g + i of column n of batch
-    // group bg; tiles q < DM hold Re of modes 16 q + 4 g + i, tiles DM + q Im
-    f32x4 X[NBG][2 * DM];
+    for (int k = 0; k < CPW; ++k)
 #pragma unroll
-    for (int bg = 0; bg < NBG; ++bg)
+        for (int bg = 0; bg < NBG; ++bg)
 #pragma unroll
-        for (int mt = 0; mt < 2 * DM; ++mt) X[bg][mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+            for (int mt = 0; mt < 2 * DM; ++mt) X[k][bg][mt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
     const int64_t nch = (T + kC - 1) / kC;
 
-    // ---- u staging: item p (< kPairs) = row p / 16, steps 2 (p % 16) + {0, 1}
-    uint4 R0[kPPT][2][kRaw];
-    // Loads are unconditional, from addresses clamped into the tensor, so that
-    // no control flow surrounds the destination registers and the loads stay
-    // in flight until their data is staged two chunks later; rows and steps
-    // outside the tensor are zeroed then.
-    auto item_ok = [&](int64_t kk, int j, int h) {
-        const int p = tid + j * kThreads;
-        return p < kPairs && b0 + p / 16 < B && kk * kC + 2 * (p % 16) + h < T;
+    // ---- u staging: item p = tid + j kThreads holds (row p / (16 PPR), steps
+    // 2 ((p / PPR) % 16) + {0, 1}, channels c0 + CPP (p % PPR) ..).  Loads are
+    // unconditional, from addresses clamped into the tensor, so that no
+    // control flow surrounds the destination registers; rows, steps and
+    // channels outside the tensor are zeroed when the tile is staged.
+    auto item_of = [&](int j, int& ip, int& itp, int& irb) {
+        const int p = min(tid + j * kThreads, NITEM - 1);
+        ip = p % PPR;
+        itp = (p / PPR) % (kC / 2);
+        irb = p / (PPR * (kC / 2));
     };
-    // per-item source of chunk 0 (rows clamped into the tensor)
-    const IO* src0[kPPT];
+    const IO* src0[IPT];
 #pragma unroll
-    for (int j = 0; j < kPPT; ++j) {
-        const int p = tid + j * kThreads < kPairs ? tid + j * kThreads : kPairs - 1;
-        const int bb = b0 + p / 16 < B ? b0 + p / 16 : B - 1;
-        src0[j] = u + (int64_t(bb) * T + 2 * (p % 16)) * D + c0;
+    for (int j = 0; j < IPT; ++j) {
+        int ip, itp, irb;
+        item_of(j, ip, itp, irb);
+        src0[j] = u + (int64_t(min(b0 + irb, B - 1)) * T + 2 * itp) * D +
+                  min(c0 + ip * CPP, D - CPP);
     }
-    auto load_tile = [&](int64_t kk, uint4 (&Rg)[kPPT][2][kRaw]) {
-        if ((kk + 1) * kC <= T) {  // full chunk: every step in range (uniform branch)
+    uint4 R0[IPT][2];
+    auto load_tile = [&](int64_t kk) {
+        if ((kk + 1) * kC <= T) {  // full chunk (uniform branch)
             const int64_t off = kk * kC * D;
 #pragma unroll
-            for (int j = 0; j < kPPT; ++j)
+            for (int j = 0; j < IPT; ++j)
 #pragma unroll
-                for (int h = 0; h < 2; ++h) {
-                    const uint4* src = reinterpret_cast<const uint4*>(src0[j] + off + h * D);
-#pragma unroll
-                    for (int v = 0; v < kRaw; ++v) Rg[j][h][v] = src[v];
-                }
+                for (int h = 0; h < 2; ++h)
+                    R0[j][h] = *reinterpret_cast<const uint4*>(src0[j] + off + h * D);
         } else {  // last chunk: steps clamped to T - 1
 #pragma unroll
-            for (int j = 0; j < kPPT; ++j) {
-                const int p = tid + j * kThreads < kPairs ? tid + j * kThreads : kPairs - 1;
+            for (int j = 0; j < IPT; ++j) {
+                int ip, itp, irb;
+                item_of(j, ip, itp, irb);
 #pragma unroll
                 for (int h = 0; h < 2; ++h) {
-                    const int64_t t = kk * kC + 2 * (p % 16) + h;
-                    const int64_t tc = (t < T ? t : T - 1) - 2 * (p % 16);
-                    const uint4* src = reinterpret_cast<const uint4*>(src0[j] + tc * D);
-#pragma unroll
-                    for (int v = 0; v < kRaw; ++v) Rg[j][h][v] = src[v];
+                    const int64_t t = kk * kC + 2 * itp + h;
+                    const int64_t tc = (t < T ? t : T - 1) - 2 * itp;
+                    R0[j][h] = *reinterpret_cast<const uint4*>(src0[j] + tc * D);
                 }
             }
         }
     };
-    auto store_tile = [&](int64_t kk, int buf, const uint4 (&Rg)[kPPT][2][kRaw]) {
+    auto store_tile = [&](int64_t kk) {
 #pragma unroll
-        for (int j = 0; j < kPPT; ++j) {
-            const int p = tid + j * kThreads;
-            if (p >= kPairs) continue;
-            const int rb = p / 16, sp = p % 16;
-            const bool ok0 = item_ok(kk, j, 0), ok1 = item_ok(kk, j, 1);
+        for (int j = 0; j < IPT; ++j) {
+            if (tid + j * kThreads >= NITEM) continue;
+            int ip, itp, irb;
+            item_of(j, ip, itp, irb);
+            const bool in = b0 + irb < B && c0 + ip * CPP < D;
+            const bool ok0 = in && kk * kC + 2 * itp < T;
+            const bool ok1 = in && kk * kC + 2 * itp + 1 < T;
 #pragma unroll
-            for (int ch = 0; ch < kW; ++ch) {
-                const int e = (ch * BN + rb) * kC + 2 * sp;  // element of step 2 sp
-                if constexpr (sizeof(IO) == 2) {
-                    const uint32_t w0 = ok0 ? reinterpret_cast<const uint32_t*>(&Rg[j][0][0])[ch / 2] : 0u;
-                    const uint32_t w1 = ok1 ? reinterpret_cast<const uint32_t*>(&Rg[j][1][0])[ch / 2] : 0u;
+            for (int ch = 0; ch < CPP; ++ch) {
+                const int e = ((ip * CPP + ch) * BN + irb) * US + 2 * itp;  // element of step 2 itp
+                if constexpr (ES == 2) {
+                    const uint32_t w0 = ok0 ? reinterpret_cast<const uint32_t*>(&R0[j][0])[ch / 2] : 0u;
+                    const uint32_t w1 = ok1 ? reinterpret_cast<const uint32_t*>(&R0[j][1])[ch / 2] : 0u;
                     const uint32_t lo = ch % 2 == 0 ? (w0 & 0xffffu) : (w0 >> 16);
                     const uint32_t hi = ch % 2 == 0 ? (w1 & 0xffffu) : (w1 >> 16);
-                    reinterpret_cast<uint32_t*>(&ubuf[buf][0])[e / 2] = lo | (hi << 16);
+                    reinterpret_cast<uint32_t*>(ubuf)[e / 2] = lo | (hi << 16);
                 } else {
-                    const float v0 = ok0 ? reinterpret_cast<const float*>(&Rg[j][0][0])[ch] : 0.f;
-                    const float v1 = ok1 ? reinterpret_cast<const float*>(&Rg[j][1][0])[ch] : 0.f;
-                    *reinterpret_cast<float2*>(&ubuf[buf][e]) = make_float2(v0, v1);
+                    const float v0 = ok0 ? reinterpret_cast<const float*>(&R0[j][0])[ch] : 0.f;
+                    const float v1 = ok1 ? reinterpret_cast<const float*>(&R0[j][1])[ch] : 0.f;
+                    *reinterpret_cast<float2*>(&ubuf[e]) = make_float2(v0, v1);
                 }
             }
         }
     };
 
-    // U operand of batch group bg: steps 8g..8g+7 of row 16 bg + n, channel w
-    auto load_u = [&](int buf, int bg, bf16x8 (&U)[NTU]) {
-        const int ue = (w * BN + kN * bg + n) * kC + 8 * g;
+    // U operand of channel k, batch group bg: steps 8g..8g+7 of row 16 bg + n
+    auto load_u = [&](int k, int bg, bf16x8 (&U)[NTU]) {
+        const int ue = ((w * CPW + k) * BN + kN * bg + n) * US + 8 * g;
         if constexpr (NTU == 1) {
-            U[0] = *reinterpret_cast<const bf16x8*>(&ubuf[buf][ue]);
+            U[0] = *reinterpret_cast<const bf16x8*>(&ubuf[ue]);
         } else {
-            const float4 lo = *reinterpret_cast<const float4*>(&ubuf[buf][ue]);
-            const float4 hi = *reinterpret_cast<const float4*>(&ubuf[buf][ue + 4]);
+            const float4 lo = *reinterpret_cast<const float4*>(&ubuf[ue]);
+            const float4 hi = *reinterpret_cast<const float4*>(&ubuf[ue + 4]);
             const float uv[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
 #pragma unroll
             for (int i = 0; i < 8; ++i) {
@@ -344,64 +392,80 @@ __global__ __launch_bounds__(kThreads) void mfma_prefill_kernel(
             }
         }
     };
-    // X_in of batch group bg as the B operand of W X_in (K index 8g + i <->
-    // tile q (i < 4), tile DM + q (i >= 4)) in two bfloat16 terms: the
-    // correction W X_in then carries a relative error near 2^-16 while the
-    // carried state itself stays float32
-    auto split_x = [&](int bg, bf16x8 (&XB)[DM][2]) {
+    // X_in as the B operand of W X_in (K index 8g + i <-> tile q (i < 4),
+    // tile DM + q (i >= 4)) in two bfloat16 terms: the correction W X_in then
+    // carries a relative error near 2^-16 while the carried state itself
+    // stays float32
+    auto split_x = [&](const f32x4 (&Xs)[2 * DM], bf16x8 (&XB)[DM][2]) {
 #pragma unroll
         for (int q = 0; q < DM; ++q)
 #pragma unroll
             for (int i = 0; i < 8; ++i) {
-                const float v = i < 4 ? X[bg][q][i] : X[bg][DM + q][i - 4];
+                const float v = i < 4 ? Xs[q][i] : Xs[DM + q][i - 4];
                 const __bf16 a = static_cast<__bf16>(v);
                 XB[q][0][i] = a;
                 XB[q][1][i] = static_cast<__bf16>(v - static_cast<float>(a));
             }
     };
-    // Y = T U + W X_in of batch group bg into the output stage
-    auto stage_y = [&](int bg, const f32x4 (&Y)[2]) {
+    // word of the y stage holding word dw (< SD) of (row, step)
+    auto ysw = [&](int row, int step, int dw) { return row * RS + step * SD + (dw ^ ((step >> 2) & 3)); };
+    // Y (row 16 bg + n, steps 16 mt + 4 g + i) of this wave's CPW channels
+    // into the output stage, adjacent bfloat16 channels packed into one word
+    auto stage_y = [&](int bg, const f32x4 (&Y)[CPW][2]) {
 #pragma unroll
         for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
-            for (int i = 0; i < 4; ++i)
-                io_store(&ystage[(kN * bg + n) * kYRow + (16 * mt + 4 * g + i) * kW + w], Y[mt][i]);
+            for (int i = 0; i < 4; ++i) {
+                const int row = kN * bg + n, step = 16 * mt + 4 * g + i;
+                if constexpr (ES == 2 && CPW == 2) {
+                    const uint32_t lo = __builtin_bit_cast(uint16_t, static_cast<__bf16>(Y[0][mt][i]));
+                    const uint32_t hi = __builtin_bit_cast(uint16_t, static_cast<__bf16>(Y[1][mt][i]));
+                    ystage[ysw(row, step, w)] = lo | (hi << 16);
+                } else if constexpr (ES == 2) {  // one bfloat16 channel: half word w % 2 of word w / 2
+                    io_store(reinterpret_cast<IO*>(ystage) + 2 * ysw(row, step, w / 2) + w % 2,
+                             Y[0][mt][i]);
+                } else {
+                    reinterpret_cast<float*>(ystage)[ysw(row, step, w)] = Y[0][mt][i];
+                }
+            }
     };
-    constexpr int kWX = 4;  // (A term, X term) pairs of W X_in: (0,0) (0,1) (1,0) (2,0)
-    constexpr int kWXa[kWX] = {0, 0, 1, 2};
-    constexpr int kWXx[kWX] = {0, 1, 0, 0};
-    constexpr int G = NBG < 2 ? NBG : 2;  // batch groups whose MFMA chains interleave
+    // (A term, X term) pairs of W X_in: (0,0) (0,1) (1,0), and (2,0) with
+    // three-term A operands
+    constexpr int kWX = KT == 2 ? 3 : 4;
+    constexpr int kWXa[4] = {0, 0, 1, 2};
+    constexpr int kWXx[4] = {0, 1, 0, 0};
 
-    // full chunk: for G batch groups at a time, every product term is issued
-    // for all independent accumulators (2 Y tiles and 2 DM S tiles per group)
-    auto compute_full = [&](int buf) {
+    // full chunk, one batch group at a time: every product term is issued
+    // for all independent accumulators of the wave's channels (2 Y tiles and
+    // 2 DM S tiles per channel), then the carry and the output stage
+    auto compute_full = [&]() {
 #pragma unroll
-        for (int bp = 0; bp < NBG; bp += G) {
-            bf16x8 U[G][NTU];
-            bf16x8 XB[G][DM][2];
-            f32x4 Y[G][2], Sr[G][DM], Si[G][DM];
+        for (int bg = 0; bg < NBG; ++bg) {
+            bf16x8 U[CPW][NTU];
+            bf16x8 XB[CPW][DM][2];
+            f32x4 Y[CPW][2], Sr[CPW][DM], Si[CPW][DM];
 #pragma unroll
-            for (int gg = 0; gg < G; ++gg) {
-                load_u(buf, bp + gg, U[gg]);
-                split_x(bp + gg, XB[gg]);
-                Y[gg][0] = Y[gg][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+            for (int k = 0; k < CPW; ++k) {
+                load_u(k, bg, U[k]);
+                split_x(X[k][bg], XB[k]);
+                Y[k][0] = Y[k][1] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-                for (int q = 0; q < DM; ++q) Sr[gg][q] = Si[gg][q] = f32x4{0.f, 0.f, 0.f, 0.f};
+                for (int q = 0; q < DM; ++q) Sr[k][q] = Si[k][q] = f32x4{0.f, 0.f, 0.f, 0.f};
             }
 #pragma unroll
-            for (int ia = 0; ia < kTerms; ++ia)
+            for (int ia = 0; ia < KT; ++ia)
 #pragma unroll
                 for (int ju = 0; ju < NTU; ++ju) {
-                    if (ia + ju >= kTerms) continue;
+                    if (ia + ju >= KT) continue;
 #pragma unroll
-                    for (int gg = 0; gg < G; ++gg) {
+                    for (int k = 0; k < CPW; ++k) {
 #pragma unroll
                         for (int mt = 0; mt < 2; ++mt)
-                            Y[gg][mt] = mfma(A[2 * DM + mt][ia], U[gg][ju], Y[gg][mt]);
+                            Y[k][mt] = mfma(A[k][2 * DM + mt][ia], U[k][ju], Y[k][mt]);
 #pragma unroll
                         for (int q = 0; q < DM; ++q) {
-                            Sr[gg][q] = mfma(A[q][ia], U[gg][ju], Sr[gg][q]);
-                            Si[gg][q] = mfma(A[DM + q][ia], U[gg][ju], Si[gg][q]);
+                            Sr[k][q] = mfma(A[k][q][ia], U[k][ju], Sr[k][q]);
+                            Si[k][q] = mfma(A[k][DM + q][ia], U[k][ju], Si[k][q]);
                         }
                     }
                 }
@@ -410,83 +474,96 @@ __global__ __launch_bounds__(kThreads) void mfma_prefill_kernel(
 #pragma unroll
                 for (int q = 0; q < DM; ++q)
 #pragma unroll
-                    for (int gg = 0; gg < G; ++gg)
+                    for (int k = 0; k < CPW; ++k)
 #pragma unroll
                         for (int mt = 0; mt < 2; ++mt)
-                            Y[gg][mt] = mfma(A[2 * DM + 2 + mt * DM + q][kWXa[p]],
-                                             XB[gg][q][kWXx[p]], Y[gg][mt]);
+                            Y[k][mt] = mfma(A[k][2 * DM + 2 + mt * DM + q][kWXa[p]],
+                                            XB[k][q][kWXx[p]], Y[k][mt]);
 #pragma unroll
-            for (int gg = 0; gg < G; ++gg) {
-                stage_y(bp + gg, Y[gg]);
+            for (int k = 0; k < CPW; ++k)
 #pragma unroll
                 for (int q = 0; q < DM; ++q)
 #pragma unroll
                     for (int i = 0; i < 4; ++i) {  // carry: X <- lambda^C X + S
-                        const float xr = X[bp + gg][q][i], xi = X[bp + gg][DM + q][i];
-                        X[bp + gg][q][i] = fmaf(lcr[q][i], xr, fmaf(-lci[q][i], xi, Sr[gg][q][i]));
-                        X[bp + gg][DM + q][i] = fmaf(lcr[q][i], xi, fmaf(lci[q][i], xr, Si[gg][q][i]));
+                        const float2 l = lcs[w * CPW + k][g][4 * q + i];
+                        const float xr = X[k][bg][q][i], xi = X[k][bg][DM + q][i];
+                        X[k][bg][q][i] = fmaf(l.x, xr, fmaf(-l.y, xi, Sr[k][q][i]));
+                        X[k][bg][DM + q][i] = fmaf(l.x, xi, fmaf(l.y, xr, Si[k][q][i]));
                     }
-            }
+            stage_y(bg, Y);
         }
     };
 
     // last, partial chunk of tr < C steps: outputs as above (the staged
     // inputs past T are zero), end state by the recurrence over its inputs
-    auto compute_partial = [&](int buf, int tr) {
+    auto compute_partial = [&](int tr) {
 #pragma unroll
         for (int bg = 0; bg < NBG; ++bg) {
-            bf16x8 U[NTU];
-            bf16x8 XB[DM][2];
-            load_u(buf, bg, U);
-            split_x(bg, XB);
-            f32x4 Y[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
+            f32x4 Y[CPW][2];
 #pragma unroll
-            for (int mt = 0; mt < 2; ++mt) {
+            for (int k = 0; k < CPW; ++k) {
+                bf16x8 U[NTU];
+                bf16x8 XB[DM][2];
+                load_u(k, bg, U);
+                split_x(X[k][bg], XB);
 #pragma unroll
-                for (int ia = 0; ia < kTerms; ++ia)
+                for (int mt = 0; mt < 2; ++mt) {
+                    Y[k][mt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-                    for (int ju = 0; ju < NTU; ++ju)
-                        if (ia + ju < kTerms) Y[mt] = mfma(A[2 * DM + mt][ia], U[ju], Y[mt]);
+                    for (int ia = 0; ia < KT; ++ia)
 #pragma unroll
-                for (int p = 0; p < kWX; ++p)
+                        for (int ju = 0; ju < NTU; ++ju)
+                            if (ia + ju < KT) Y[k][mt] = mfma(A[k][2 * DM + mt][ia], U[ju], Y[k][mt]);
 #pragma unroll
-                    for (int q = 0; q < DM; ++q)
-                        Y[mt] = mfma(A[2 * DM + 2 + mt * DM + q][kWXa[p]], XB[q][kWXx[p]], Y[mt]);
+                    for (int p = 0; p < kWX; ++p)
+#pragma unroll
+                        for (int q = 0; q < DM; ++q)
+                            Y[k][mt] = mfma(A[k][2 * DM + 2 + mt * DM + q][kWXa[p]],
+                                            XB[q][kWXx[p]], Y[k][mt]);
+                }
             }
             stage_y(bg, Y);
-            const int ue0 = (w * BN + kN * bg + n) * kC;
+        }
 #pragma unroll
-            for (int q = 0; q < DM; ++q)
+        for (int k = 0; k < CPW; ++k) {
+            const int cc = min(c0 + w * CPW + k, D - 1);
 #pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const float2 l1 = lam[int64_t(c) * d + 16 * q + 4 * g + i];
-                    float xr = X[bg][q][i], xi = X[bg][DM + q][i];
-                    for (int j = 0; j < tr; ++j) {
-                        const float uv = static_cast<float>(ubuf[buf][ue0 + j]);
-                        const float nr = fmaf(l1.x, xr, fmaf(-l1.y, xi, uv));
-                        xi = fmaf(l1.x, xi, l1.y * xr);
-                        xr = nr;
+            for (int bg = 0; bg < NBG; ++bg) {
+                const int ue0 = ((w * CPW + k) * BN + kN * bg + n) * US;
+#pragma unroll
+                for (int q = 0; q < DM; ++q)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        const float2 l1 = lam[int64_t(cc) * d + 16 * q + 4 * g + i];
+                        float xr = X[k][bg][q][i], xi = X[k][bg][DM + q][i];
+                        for (int j = 0; j < tr; ++j) {
+                            const float uv = static_cast<float>(ubuf[ue0 + j]);
+                            const float nr = fmaf(l1.x, xr, fmaf(-l1.y, xi, uv));
+                            xi = fmaf(l1.x, xi, l1.y * xr);
+                            xr = nr;
+                        }
+                        X[k][bg][q][i] = xr;
+                        X[k][bg][DM + q][i] = xi;
                     }
-                    X[bg][q][i] = xr;
-                    X[bg][DM + q][i] = xi;
-                }
+            }
         }
     };
 
-    // stage -> y: item r = row r / kC, step r % kC (8 channels, 16-byte stores)
+    // stage -> y: piece r = row r / (kC PPR), step (r / PPR) % kC, channels
+    // c0 + CPP (r % PPR) ..
     auto write_y = [&](int64_t kk) {
         const int64_t t0 = kk * kC;
 #pragma unroll
-        for (int j = 0; j < (BN * kC + kThreads - 1) / kThreads; ++j) {
+        for (int j = 0; j < (NYP + kThreads - 1) / kThreads; ++j) {
             const int r = tid + j * kThreads;
-            const int rb = r / kC, rt = r % kC;
+            const int rp = r % PPR, rt = (r / PPR) % kC, rb = r / (PPR * kC);
             const int64_t gt = t0 + rt;
-            if (r < BN * kC && b0 + rb < B && gt < T) {
-                const uint32_t* src = reinterpret_cast<const uint32_t*>(&ystage[rb * kYRow + rt * kW]);
-                uint4* dst = reinterpret_cast<uint4*>(y + (int64_t(b0 + rb) * T + gt) * D + c0);
-#pragma unroll
-                for (int v = 0; v < kRaw; ++v)
-                    dst[v] = make_uint4(src[4 * v], src[4 * v + 1], src[4 * v + 2], src[4 * v + 3]);
+            if (r < NYP && b0 + rb < B && gt < T && c0 + rp * CPP < D) {
+                uint4 v = *reinterpret_cast<const uint4*>(&ystage[rb * RS + rt * SD + 4 * rp]);
+                const int f = (rt >> 2) & 3;  // undo the word permutation of the piece
+                if (f & 1) v = make_uint4(v.y, v.x, v.w, v.z);
+                if (f & 2) v = make_uint4(v.z, v.w, v.x, v.y);
+                *reinterpret_cast<uint4*>(y + (int64_t(b0 + rb) * T + gt) * D + c0 + rp * CPP) = v;
             }
         }
     };
@@ -499,49 +576,65 @@ __global__ __launch_bounds__(kThreads) void mfma_prefill_kernel(
     // loads issued a whole compute phase before.  The last, partial chunk is
     // handled after the loop, so that the loop body holds no other path.
     const int64_t nfull = T / kC;
-    auto step_full = [&](int64_t kk) {
-        compute_full(0);
-        lds_barrier();  // tile consumed, stage complete
-        if (kk + 1 < nch) store_tile(kk + 1, 0, R0);
-        write_y(kk);
-        if (kk + 2 < nch) load_tile(kk + 2, R0);
-        lds_barrier();  // next tile staged, stage free
-    };
-
-    load_tile(0, R0);
-    store_tile(0, 0, R0);
-    if (nch > 1) load_tile(1, R0);
+    load_tile(0);
+    store_tile(0);
+    if (nch > 1) load_tile(1);
     lds_barrier();
-    for (int64_t kk = 0; kk < nfull; ++kk) step_full(kk);
+    for (int64_t kk = 0; kk < nfull; ++kk) {
+        compute_full();
+        lds_barrier();  // tile consumed, stage complete
+        if (kk + 1 < nch) store_tile(kk + 1);
+        write_y(kk);
+        if (kk + 2 < nch) load_tile(kk + 2);
+        lds_barrier();  // next tile staged, stage free
+    }
     if (nch > nfull) {  // chunk nfull (staged)
-        compute_partial(0, int(T - nfull * kC));
+        compute_partial(int(T - nfull * kC));
         lds_barrier();
         write_y(nfull);
     }
 
     // ---- x_T
 #pragma unroll
-    for (int bg = 0; bg < NBG; ++bg) {
-        const int b = b0 + kN * bg + n;
-        if (b < B) {
-            float2* dst = state + (int64_t(b) * D + c) * d;
+    for (int k = 0; k < CPW; ++k) {
+        const int c = c0 + w * CPW + k;
 #pragma unroll
-            for (int q = 0; q < DM; ++q)
+        for (int bg = 0; bg < NBG; ++bg) {
+            const int b = b0 + kN * bg + n;
+            if (b < B && c < D) {
+                float2* dst = state + (int64_t(b) * D + c) * d;
 #pragma unroll
-                for (int i = 0; i < 4; ++i)
-                    dst[16 * q + 4 * g + i] = make_float2(X[bg][q][i], X[bg][DM + q][i]);
+                for (int q = 0; q < DM; ++q)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i)
+                        dst[16 * q + 4 * g + i] = make_float2(X[k][bg][q][i], X[k][bg][DM + q][i]);
+            }
         }
     }
 }
 
-// batch groups of 16 rows per workgroup
+// batch groups of 16 rows per wave: two when there are more than 16 rows and
+// the registers allow (float32 inputs with d = 16, one channel per wave)
 int mfma_nbg(int64_t B, int64_t d, bool bf16_io)
 {
-    if (d != 16) return 1;
-    const int cap = 2;  // four groups exceed the register file (the prefetch would spill)
-    int nbg = 1;
-    while (nbg < cap && B > 16 * nbg) nbg *= 2;
-    return nbg;
+    return d == 16 && !bf16_io && B > kN ? 2 : 1;
+}
+
+template <typename IO, int DM, int NBG>
+hipError_t launch_main(const float2* lam, const void* u, void* y, float2* state,
+                       const bf16x8* frag, const float2* lamc, int64_t B, int64_t D, int64_t T,
+                       hipStream_t stream)
+{
+    constexpr int CW = kW * Tiling<IO, DM>::CPW;
+    const int64_t ncg = (D + CW - 1) / CW;
+    const int64_t nbg = (B + kN * NBG - 1) / (kN * NBG);
+    const int64_t per_xcd = (ncg * nbg + 7) / 8;  // logical workgroups per XCD
+    const int64_t grid = 8 * per_xcd;
+    if (grid > 0x7fffffff) return hipErrorInvalidConfiguration;
+    hipLaunchKernelGGL((mfma_prefill_kernel<IO, DM, NBG>), dim3(uint32_t(grid)), dim3(kThreads),
+                       0, stream, lam, static_cast<const IO*>(u), static_cast<IO*>(y), state,
+                       frag, lamc, int(B), int(D), T, int(ncg), int(nbg), int(per_xcd));
+    return hipGetLastError();
 }
 
 }  // namespace
@@ -562,11 +655,13 @@ bool mfma_supported(int64_t B, int64_t D, int64_t d, int64_t T)
 }
 
 // The matrix-core plan has no parallelism along time: the automatic plan takes
-// it when the (channel group, 32-row batch block) pairs alone fill the GPU.
+// it when its workgroups alone fill the GPU, counted as 16 channels x 32 batch
+// rows (two rounds of the bfloat16 tiling with d = 16, 16 x 16).  The choice must not depend on the
+// input type, which the workspace query does not know.
 bool mfma_preferred(int64_t B, int64_t D, int64_t d)
 {
     (void)d;
-    return (D / kW) * ((B + 31) / 32) >= kMinWorkgroups;
+    return ((D + 15) / 16) * ((B + 31) / 32) >= kMinWorkgroups;
 }
 
 hipError_t launch_prefill_mfma(const float2* lam, const float2* R, const float* h0,
@@ -580,14 +675,7 @@ hipError_t launch_prefill_mfma(const float2* lam, const float2* R, const float* 
     bf16x8* frag = static_cast<bf16x8*>(workspace);
     float2* lamc = reinterpret_cast<float2*>(static_cast<char*>(workspace) +
                                              (frag_bytes + 255) / 256 * 256);
-    const int nbgw = mfma_nbg(B, d, bf16_io);  // batch groups per workgroup
-    const int ncg = int(D / kW);
-    const int nbg = int((B + 16 * nbgw - 1) / (16 * nbgw));
-    const int nlg = (ncg + 7) / 8;
-    const int64_t groups = int64_t(nlg) * nbg;     // (line group, batch block) pairs
-    const int64_t per_xcd = (groups + 7) / 8 * 8;  // logical slots per XCD
-    const int64_t grid = 8 * per_xcd;
-    if (D > 0x7fffffff || grid > 0x7fffffff) return hipErrorInvalidConfiguration;
+    if (D > 0x7fffffff) return hipErrorInvalidConfiguration;
     if (DM == 1)
         hipLaunchKernelGGL(mfma_setup_kernel<1>, dim3(uint32_t(D)), dim3(256), 0, stream, lam,
                            R, h0, frag, lamc);
@@ -596,22 +684,13 @@ hipError_t launch_prefill_mfma(const float2* lam, const float2* R, const float* 
                            R, h0, frag, lamc);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-#define LH_MFMA(IO, DMV, NBGV)                                                                  \
-    hipLaunchKernelGGL((mfma_prefill_kernel<IO, DMV, NBGV>), dim3(uint32_t(grid)),             \
-                       dim3(kThreads), 0, stream, lam, static_cast<const IO*>(u),               \
-                       static_cast<IO*>(y), state, frag, lamc, int(B), int(D), T, ncg, nbg, nlg, \
-                       int(per_xcd))
-    if (bf16_io) {
-        if (DM == 2) LH_MFMA(bf16, 2, 1);
-        else if (nbgw == 2) LH_MFMA(bf16, 1, 2);
-        else LH_MFMA(bf16, 1, 1);
-    } else {
-        if (DM == 2) LH_MFMA(float, 2, 1);
-        else if (nbgw == 2) LH_MFMA(float, 1, 2);
-        else LH_MFMA(float, 1, 1);
-    }
-#undef LH_MFMA
-    return hipGetLastError();
+    const bool two = mfma_nbg(B, d, bf16_io) == 2;
+    if (bf16_io)
+        return DM == 2 ? launch_main<bf16, 2, 1>(lam, u, y, state, frag, lamc, B, D, T, stream)
+                       : launch_main<bf16, 1, 1>(lam, u, y, state, frag, lamc, B, D, T, stream);
+    if (DM == 2) return launch_main<float, 2, 1>(lam, u, y, state, frag, lamc, B, D, T, stream);
+    return two ? launch_main<float, 1, 2>(lam, u, y, state, frag, lamc, B, D, T, stream)
+               : launch_main<float, 1, 1>(lam, u, y, state, frag, lamc, B, D, T, stream);
 }
 
 }  // namespace lh
