@@ -58,18 +58,23 @@ def src_digest(*names):
     return h.hexdigest()[:16]
 
 
-def counter_traffic(summary_name, digest):
-    """HBM bytes per launch from a committed rocprofv3 counter summary, if it
-    was taken on the current kernel source (else None)."""
+def profile_value(summary_name, key, digest):
+    """A figure from a committed rocprofv3 counter summary, if the summary was
+    taken on the current kernel source (else None)."""
     path = os.path.join(PROFILES, summary_name)
     if not os.path.exists(path):
         return None
     text = open(path).read()
     m_src = re.search(r"^source_sha256_16:\s*([0-9a-f]+)", text, re.M)
-    m_b = re.search(r"^hbm_bytes_per_launch:\s*([0-9.eE+]+)", text, re.M)
-    if not m_src or not m_b or m_src.group(1) != digest:
+    m_v = re.search(r"^" + key + r":\s*([0-9.eE+-]+)", text, re.M)
+    if not m_src or not m_v or m_src.group(1) != digest:
         return None
-    return float(m_b.group(1))
+    return float(m_v.group(1))
+
+
+def counter_traffic(summary_name, digest):
+    """HBM bytes per launch from a committed rocprofv3 counter summary."""
+    return profile_value(summary_name, "hbm_bytes_per_launch", digest)
 
 
 def copy_calibration():
@@ -238,8 +243,8 @@ def main():
     pre_tf = prefill_flops(w) / (pre_avg * 1e-3) / 1e12
     traffic = counter_traffic(f"decode_step_{w.name}_counters.txt",
                               src_digest("decode.hip", "lh_internal.hpp"))
-    traffic_pre = counter_traffic(f"prefill_{w.name}_counters.txt",
-                                  src_digest("prefill.hip", "prefill_mfma.hip", "lh_internal.hpp"))
+    pre_digest = src_digest("prefill.hip", "prefill_mfma.hip", "lh_internal.hpp")
+    traffic_pre = counter_traffic(f"prefill_{w.name}_counters.txt", pre_digest)
 
     # HBM-streaming decode: the same kernel over a pool of state buffers larger
     # than the 256 MB Infinity Cache (like the layers of a model), so every
@@ -300,7 +305,11 @@ def main():
                              "unit": "TFLOP/s", "frac": pre_tf / FP32_VALU_PEAK_TFLOPS,
                              "traffic": traffic_pre, "flops_per_launch": prefill_flops(w),
                              "bytes_per_launch": prefill_bytes(w),
-                             "gbps": prefill_bytes(w) / (pre_avg * 1e-3) / 1e9},
+                             "gbps": prefill_bytes(w) / (pre_avg * 1e-3) / 1e9,
+                             "mfma_busy": profile_value(f"prefill_{w.name}_sq_counters.txt",
+                                                        "mfma_busy_fraction", pre_digest),
+                             "valu_busy": profile_value(f"prefill_{w.name}_sq_counters.txt",
+                                                        "valu_busy_fraction", pre_digest)},
         "decode_hbm_streaming": streaming,
         "cpu_baseline": cpu,
         "setup_s": setup_s,
