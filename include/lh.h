@@ -155,6 +155,34 @@ lh_status lh_step(const lh_c32* lambda, const lh_c32* R, const float* h0,
                   int64_t B, int64_t D, int64_t d, lh_dtype io_dtype,
                   void* stream);
 
+/*
+ * Multi-head decode step (Sec. 5, "Multi-head Long Convolutions": the
+ * projections q, k, v of width D = M N are split into M heads of N channels;
+ * per head the outer product z = k (x) v is convolved entry by entry with the
+ * head's distilled filter and the result multiplies q).  Every entry (i, j)
+ * of head m carries the d-mode state of Proposition "modal_realization":
+ *
+ *   z[i,j]          = k[b, mN+i] v[b, mN+j]
+ *   y[b, mN+i]      = sum_j q[b, mN+j] ( Re(sum_n R[m,n] state[b,m,i,j,n])
+ *                                        + h0[m] z[i,j] )          (reads state)
+ *   state[b,m,i,j,n] = lambda[m,n] state[b,m,i,j,n] + z[i,j]       (in place)
+ *
+ * The q contraction runs over the second (value) index of z; exchanging the
+ * k and v arguments gives the other orientation (q against the key index).
+ *
+ *   lambda, R : [M, d] complex64;  h0 : [M] float32 (one filter per head)
+ *   state     : in/out [B, M, N, N, d] complex64, mode fastest
+ *   q, k, v   : [B, M N] (io_dtype);  y : out [B, M N] (io_dtype)
+ *   B, M, N   : >= 1;  1 <= d <= LH_MAX_MODES
+ * y must not overlap any other buffer; state must not overlap lambda, R, h0,
+ * q, k or v.  One kernel launch; no workspace; same execution and error
+ * rules as lh_step.
+ */
+lh_status lh_mh_step(const lh_c32* lambda, const lh_c32* R, const float* h0,
+                     lh_c32* state, const void* q, const void* k, const void* v, void* y,
+                     int64_t B, int64_t M, int64_t N, int64_t d, lh_dtype io_dtype,
+                     void* stream);
+
 #ifdef __cplusplus
 }
 #endif

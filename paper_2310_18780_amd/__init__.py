@@ -27,6 +27,7 @@ __all__ = [
     "workspace_bytes",
     "prefill",
     "step",
+    "mh_step",
     "STATUS",
 ]
 
@@ -83,6 +84,8 @@ def lib() -> ctypes.CDLL:
     L.lh_prefill.restype = ctypes.c_int
     L.lh_step.argtypes = [vp, vp, vp, vp, vp, vp, i64, i64, i64, ctypes.c_int, vp]
     L.lh_step.restype = ctypes.c_int
+    L.lh_mh_step.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, i64, i64, i64, i64, ctypes.c_int, vp]
+    L.lh_mh_step.restype = ctypes.c_int
     _lib = L
     return L
 
@@ -175,3 +178,25 @@ def step(lam, R, h0, state, u_t, y_t, stream=None) -> None:
     _check(lib().lh_step(lam.data_ptr(), R.data_ptr(), h0.data_ptr(), state.data_ptr(),
                          u_t.data_ptr(), y_t.data_ptr(), B, D, d, io,
                          _stream(u_t.device, stream)))
+
+
+def mh_step(lam, R, h0, state, q, k, v, y, stream=None) -> None:
+    """One multi-head decode step (``lh_mh_step``): ``y`` from the current
+    per-entry states of the ``M`` heads, then the state update in place.
+
+    ``lam``, ``R``: ``[M, d]`` complex64; ``h0``: ``[M]``; ``state``:
+    ``[B, M, N, N, d]`` complex64; ``q``, ``k``, ``v``, ``y``: ``[B, M N]``.
+    """
+    import torch
+
+    B, M, N, _, d = state.shape
+    _need(lam, "lam", torch.complex64, (M, d))
+    _need(R, "R", torch.complex64, (M, d))
+    _need(h0, "h0", torch.float32, (M,))
+    _need(state, "state", torch.complex64, (B, M, N, N, d))
+    for name, t in (("q", q), ("k", k), ("v", v), ("y", y)):
+        _need(t, name, q.dtype, (B, M * N))
+    io = _io_dtype(q)
+    _check(lib().lh_mh_step(lam.data_ptr(), R.data_ptr(), h0.data_ptr(), state.data_ptr(),
+                            q.data_ptr(), k.data_ptr(), v.data_ptr(), y.data_ptr(), B, M, N, d,
+                            io, _stream(q.device, stream)))

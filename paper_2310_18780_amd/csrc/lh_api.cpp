@@ -273,4 +273,59 @@ lh_status lh_step(const lh_c32* lambda, const lh_c32* R, const float* h0, lh_c32
                     "step launch");
 }
 
+lh_status lh_mh_step(const lh_c32* lambda, const lh_c32* R, const float* h0, lh_c32* state,
+                      const void* q, const void* k, const void* v, void* y, int64_t B,
+                      int64_t M, int64_t N, int64_t d, lh_dtype io_dtype, void* stream)
+{
+    g_last_error[0] = '\0';
+    lh_status s;
+    if (!lambda || !R || !h0 || !state || !q || !k || !v || !y)
+        return fail(LH_ERR_INVALID_ARG, "lambda, R, h0, state, q, k, v and y must not be NULL");
+    if (M < 1) return fail(LH_ERR_INVALID_ARG, "M = %lld must be >= 1", (long long)M);
+    if (N < 1) return fail(LH_ERR_INVALID_ARG, "N = %lld must be >= 1", (long long)N);
+    int64_t D = 0, rows = 0;
+    if (!mul_ok(M, N, &D)) return fail(LH_ERR_INVALID_ARG, "M * N overflows");
+    if ((s = check_sizes(B, D, d, 0)) != LH_OK) return s;
+    int64_t cells = 0;  // complex entries of the state
+    if (!mul_ok(B, D, &rows) || !mul_ok(rows, N, &cells) || !mul_ok(cells, d, &cells) ||
+        !mul_ok(cells, 8, &cells))
+        return fail(LH_ERR_INVALID_ARG, "state size overflows (B=%lld M=%lld N=%lld d=%lld)",
+                    (long long)B, (long long)M, (long long)N, (long long)d);
+    if ((s = check_dtype(io_dtype)) != LH_OK) return s;
+
+    const size_t es = io_dtype == LH_BF16 ? 2 : 4;
+    const Buf b_lam = buf("lambda", lambda, sizeof(lh_c32) * M * d);
+    const Buf b_R = buf("R", R, sizeof(lh_c32) * M * d);
+    const Buf b_h0 = buf("h0", h0, sizeof(float) * M);
+    const Buf b_q = buf("q", q, es * B * D);
+    const Buf b_k = buf("k", k, es * B * D);
+    const Buf b_v = buf("v", v, es * B * D);
+    const Buf b_state = buf("state", state, size_t(cells));
+    const Buf b_y = buf("y", y, es * B * D);
+    if ((s = check_align(b_lam, 8)) || (s = check_align(b_R, 8)) || (s = check_align(b_h0, 4)) ||
+        (s = check_align(b_state, 8)) || (s = check_align(b_q, es)) ||
+        (s = check_align(b_k, es)) || (s = check_align(b_v, es)) || (s = check_align(b_y, es)))
+        return s;
+    const Buf* ins[] = {&b_lam, &b_R, &b_h0, &b_q, &b_k, &b_v};
+    for (const Buf* i : ins) {
+        if (overlaps(b_state, *i)) return fail(LH_ERR_OVERLAP, "state overlaps %s", i->name);
+        if (overlaps(b_y, *i)) return fail(LH_ERR_OVERLAP, "y overlaps %s", i->name);
+    }
+    if (overlaps(b_y, b_state)) return fail(LH_ERR_OVERLAP, "y overlaps state");
+
+    int dev = 0;
+    if ((s = check_device(&dev)) != LH_OK) return s;
+    const Buf* all[] = {&b_lam, &b_R, &b_h0, &b_q, &b_k, &b_v, &b_state, &b_y};
+    for (const Buf* b : all)
+        if ((s = check_accessible(*b, dev)) != LH_OK) return s;
+
+    const bool aligned16 = b_lam.lo % 16 == 0 && b_R.lo % 16 == 0 && b_state.lo % 16 == 0;
+    return from_hip(lh::launch_mh_step(reinterpret_cast<const float2*>(lambda),
+                                       reinterpret_cast<const float2*>(R), h0,
+                                       reinterpret_cast<float2*>(state), q, k, v, y,
+                                       io_dtype == LH_BF16, B, M, N, d, aligned16,
+                                       static_cast<hipStream_t>(stream)),
+                    "multi-head step launch");
+}
+
 }  // extern "C"

@@ -177,3 +177,37 @@ def test_binding_raises_when_library_missing(monkeypatch, tmp_path):
     monkeypatch.setattr(lh, "_lib", None)
     with pytest.raises(ImportError):
         lh.lib()
+
+
+def mh_args(**kw):
+    a = dict(lam=A, R=A + MB, h0=A + 2 * MB, state=A + 64 * MB, q=A + 3 * MB, k=A + 4 * MB,
+             v=A + 5 * MB, y=A + 128 * MB, B=2, M=2, N=4, d=4, io=lh.LH_F32, stream=None)
+    a.update(kw)
+    return [a[k] for k in ("lam", "R", "h0", "state", "q", "k", "v", "y", "B", "M", "N", "d", "io",
+                           "stream")]
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(lam=None), 1), (dict(state=None), 1), (dict(q=None), 1), (dict(k=None), 1),
+    (dict(v=None), 1), (dict(y=None), 1),
+    (dict(B=0), 1), (dict(M=0), 1), (dict(N=-1), 1), (dict(d=0), 1), (dict(d=1025), 1),
+    (dict(B=1 << 20, M=1 << 10, N=1 << 16), 1),  # state size overflow (2^63 bytes)
+    (dict(io=5), 3),
+    (dict(y=A + 4 * MB), 2),            # y aliases k
+    (dict(state=A + 5 * MB + 8), 2),    # state overlaps v
+    (dict(y=A + 64 * MB + 64), 2),      # y overlaps state
+    (dict(q=A + 3 * MB + 2), 1),        # misaligned float32
+    (dict(R=A + MB + 4), 1),            # misaligned complex64
+])
+def test_mh_step_rejects_bad_arguments(kw, status):
+    L = lh.lib()
+    assert L.lh_mh_step(*mh_args(**kw)) == status
+    assert L.lh_last_error().decode() != ""
+
+
+def test_mh_step_reports_no_device_without_gpu():
+    if not no_gpu():
+        pytest.skip("made-up addresses are only passed through when no GPU is visible")
+    L = lh.lib()
+    assert L.lh_mh_step(*mh_args()) == 4
+    assert L.lh_mh_step(*mh_args(io=lh.LH_BF16, d=3)) == 4

@@ -16,7 +16,7 @@ import pytest
 import oracle
 import oracle.multihead as mh
 
-GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "multihead_tiny.json")
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "multihead", "tiny.json")
 
 
 def rand_heads(rng, B, L, M, N, d, r=(0.5, 0.97)):

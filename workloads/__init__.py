@@ -46,6 +46,11 @@ __all__ = [
     "make_inputs",
     "bf16_round",
     "bf16_bits",
+    "MHWorkload",
+    "MH_WORKLOADS",
+    "mh_workload",
+    "mh_params",
+    "mh_row",
 ]
 
 
@@ -168,3 +173,76 @@ def make_inputs(w: Workload):
         up[b] = prompt_row(w, b)
         ud[b] = decode_row(w, b)
     return lam, R, h0, up, ud
+
+
+# ----------------------------------------------------------------------------
+# multi-head (head-tied) decode: M heads of N channels (D = M N), one distilled
+# filter per head, an N x N grid of entries per head (Sec. 5 of the paper)
+# ----------------------------------------------------------------------------
+
+@dataclasses.dataclass(frozen=True)
+class MHWorkload:
+    """``B`` sequences through one multi-head layer of width ``D = M N``: ``T0``
+    prompt steps (whose state starts the decode; 0 = an empty prompt) and
+    ``K`` decode steps."""
+
+    name: str
+    B: int
+    M: int
+    N: int
+    d: int
+    T0: int
+    K: int
+    io: str
+    r_lo: float
+    r_hi: float
+    theta_hi: float
+    r_var: float
+    seed: int = 0
+
+    @property
+    def D(self) -> int:
+        return self.M * self.N
+
+    def with_(self, **kw) -> "MHWorkload":
+        return dataclasses.replace(self, **kw)
+
+
+# Eight heads as in the paper's multi-head models, at the 355M width
+# (D = 1024, N = 128), d = 16: a 256 MiB state for 16 sequences.
+MH_WORKLOADS: Dict[str, MHWorkload] = {
+    w.name: w
+    for w in (
+        MHWorkload("mh_b16_d1024_m8_n16", 16, 8, 128, 16, 0, 64, "f32", 0.9, 0.9999, math.pi, 1.0 / 16),
+    )
+}
+
+
+def mh_workload(name: str) -> MHWorkload:
+    return MH_WORKLOADS[{"mh": "mh_b16_d1024_m8_n16"}.get(name, name)]
+
+
+def mh_params(w: MHWorkload) -> Tuple[np.ndarray, np.ndarray, np.ndarray]:
+    """Per-head filters ``(lam [M,d], R [M,d], h0 [M])``, drawn as in
+    ``make_params`` with one filter per head."""
+    rng = np.random.default_rng(w.seed)
+    r = rng.uniform(w.r_lo, w.r_hi, size=(w.M, w.d))
+    theta = rng.uniform(0.0, w.theta_hi, size=(w.M, w.d))
+    s = math.sqrt(w.r_var / 2.0)
+    re_r = rng.standard_normal((w.M, w.d)) * s
+    im_r = rng.standard_normal((w.M, w.d)) * s
+    h0 = rng.standard_normal(w.M).astype(np.float32)
+    return (r * np.exp(1j * theta)).astype(np.complex64), (re_r + 1j * im_r).astype(np.complex64), h0
+
+
+def mh_row(w: MHWorkload, b: int) -> Tuple[np.ndarray, np.ndarray, np.ndarray]:
+    """``q, k, v`` of batch element ``b`` for all ``T0 + K`` steps: float32
+    ``[T0 + K, M, N]`` each, drawn from ``default_rng([seed, 3, b])`` in the
+    order q, k, v (bfloat16-exact when ``w.io == "bf16"``)."""
+    rng = np.random.default_rng([w.seed, 3, b])
+    L = w.T0 + w.K
+    out = []
+    for _ in range(3):
+        a = rng.standard_normal((L, w.M * w.N), dtype=np.float32)
+        out.append((bf16_round(a) if w.io == "bf16" else a).reshape(L, w.M, w.N))
+    return out[0], out[1], out[2]
