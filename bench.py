@@ -47,6 +47,9 @@ def parse():
                    help="state buffers of the HBM-streaming decode measurement (0: skip)")
     p.add_argument("--copy-calibration", action="store_true",
                    help="run only a plain device copy of known size (counter calibration)")
+    p.add_argument("--multihead", action="store_true",
+                   help="time the multi-head decode step (lh_mh_step) instead, on --mh-workload")
+    p.add_argument("--mh-workload", default="mh")
     return p.parse_args()
 
 
@@ -163,6 +166,124 @@ def cpu_baseline(w, rows_wanted):
     }
 
 
+def mh_decode_bytes(w):
+    es = 2 if w.io == "bf16" else 4
+    return 16 * w.B * w.M * w.N * w.N * w.d + 4 * es * w.B * w.D + 16 * w.M * w.d + 4 * w.M
+
+
+def mh_cpu_baseline(w, seconds=10.0):
+    """The multi-head oracle on a bounded sample: complete output rows (all
+    K steps of one (b, m, i)), added in batches until about ``seconds``."""
+    import numpy as np
+
+    import oracle
+    import oracle.multihead as mho
+    import workloads
+
+    lam, R, h0 = workloads.mh_params(w)
+    q = np.empty((w.B, w.T0 + w.K, w.M, w.N), np.float32)
+    k, v = np.empty_like(q), np.empty_like(q)
+    done, bs, dt = 0, [], 0.0
+    for b in np.random.default_rng(7).permutation(w.B):
+        b = int(b)
+        q[b], k[b], v[b] = workloads.mh_row(w, b)  # input generation is not timed
+        bs.append(b)
+        order = [(b, m, i) for m in range(w.M) for i in range(w.N)]
+        for j in range(0, len(order), 64):
+            t0 = time.perf_counter()
+            mho.mh_outputs_rows(lam, R, h0, q, k, v, order[j:j + 64])
+            dt += time.perf_counter() - t0
+            done += len(order[j:j + 64])
+            if dt >= seconds:
+                break
+        if dt >= seconds:
+            break
+    return {
+        "value": done / w.D * w.K / dt,
+        "unit": "tokens/s",
+        "cores": oracle.native_threads(),
+        "kind": "oracle",
+        "sample": (f"{done} output rows (b, m, i) of {w.name} (batch rows {bs}), each all "
+                   f"T0+K={w.T0 + w.K} steps by direct float64 convolution of its N={w.N} "
+                   f"outer-product entries, in {dt:.2f} s; value = rows / D * K / time"),
+        "seconds": dt,
+    }
+
+
+def multihead_main(args):
+    import torch
+
+    import paper_2310_18780_amd as lh
+    import workloads
+
+    lh.lib()
+    w = workloads.mh_workload(args.mh_workload)
+    lam, R, h0 = (torch.from_numpy(a).cuda() for a in workloads.mh_params(w))
+    iot = torch.bfloat16 if w.io == "bf16" else torch.float32
+    L = w.T0 + w.K
+    q = torch.empty((L, w.B, w.D), dtype=iot, device="cuda")
+    k, v = torch.empty_like(q), torch.empty_like(q)
+    for b in range(w.B):
+        for dst, src in zip((q, k, v), workloads.mh_row(w, b)):
+            dst[:, b].copy_(torch.from_numpy(src.reshape(L, w.D)))
+    state = torch.zeros((w.B, w.M, w.N, w.N, w.d), dtype=torch.complex64, device="cuda")
+    y = torch.empty((w.K, w.B, w.D), dtype=iot, device="cuda")
+    for t in range(w.T0):  # the prompt's state, by stepping
+        lh.mh_step(lam, R, h0, state, q[t], k[t], v[t], y[0])
+
+    def decode_eager():
+        for t in range(w.K):
+            lh.mh_step(lam, R, h0, state, q[w.T0 + t], k[w.T0 + t], v[w.T0 + t], y[t])
+
+    decode_eager()
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        decode_eager()
+    torch.cuda.synchronize()
+    for _ in range(args.warmup):
+        graph.replay()
+    stream = torch.cuda.current_stream()
+    a, c = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    a.record(stream)
+    for _ in range(args.steps):
+        graph.replay()
+    c.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms = a.elapsed_time(c) / args.steps  # per K-step decode
+    us = ms * 1e3 / w.K
+    dbytes = mh_decode_bytes(w)
+    gbs = dbytes / (us * 1e-6) / 1e9
+    cpu = None if args.no_cpu_baseline else mh_cpu_baseline(w)
+    out = {
+        "metric": "multi-head decode tokens/s (B·steps/s) + HBM GB/s",
+        "value": w.B * w.K / (ms * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": wall * 1e3 / args.steps,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": w.name, "B": w.B, "M": w.M, "N": w.N, "D": w.D, "d": w.d,
+                   "T0": w.T0, "K": w.K, "io": w.io, "decode_launch": "graph"},
+        "decode_us_per_token_step": us,
+        "roofline": {"bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": gbs / HBM_PEAK_GBS,
+                     "traffic": counter_traffic(f"mh_step_{w.name}_counters.txt",
+                                                src_digest("multihead.hip", "lh_internal.hpp")),
+                     "kernel": "mh_step_kernel", "bytes_per_launch": dbytes},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -172,6 +293,9 @@ def main():
         sys.exit(2)
     if args.copy_calibration:
         copy_calibration()
+        return
+    if args.multihead:
+        multihead_main(args)
         return
 
     import torch
