@@ -183,6 +183,32 @@ lh_status lh_mh_step(const lh_c32* lambda, const lh_c32* R, const float* h0,
                      int64_t B, int64_t M, int64_t N, int64_t d, lh_dtype io_dtype,
                      void* stream);
 
+/*
+ * Distillation objective of the modal form (Sec. 3.2, "Modal canonical
+ * form"; the O(dL) filter evaluation of Lemma "ssmd_impulse").  Per channel c,
+ * poles in polar form lambda = A e^{i theta} and residues R (cartesian) are
+ * fitted to a real target filter h_1 .. h_L by the squared l2 interpolation
+ * error:
+ *
+ *   hhat_t = Re sum_n R[c,n] lambda[c,n]^(t-1)   (t = 1..L)
+ *   loss[c] = sum_t (hhat_t - h_t)^2
+ *
+ * with its gradients with respect to A, theta, Re R and Im R (dR holds
+ * d/dRe R + i d/dIm R).  The pass-through h0 is matched by h_0 and is not
+ * part of the objective.
+ *
+ *   A, theta : [D, d] float32 (polar poles);  R : [D, d] complex64
+ *   target   : [D, L] float32, target[c, t-1] = h_t
+ *   loss     : out [D];  dA, dtheta : out [D, d];  dR : out [D, d] complex64
+ *   hhat     : out [D, L] (the materialised filter) or NULL
+ *   D >= 1, 1 <= d <= LH_MAX_MODES, L >= 1
+ * Outputs must not overlap each other or the inputs.  One kernel launch; no
+ * workspace; same execution and error rules as lh_step.
+ */
+lh_status lh_distill(const float* A, const float* theta, const lh_c32* R, const float* target,
+                     int64_t D, int64_t d, int64_t L, float* loss, float* dA, float* dtheta,
+                     lh_c32* dR, float* hhat, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -28,6 +28,7 @@ __all__ = [
     "prefill",
     "step",
     "mh_step",
+    "distill",
     "STATUS",
 ]
 
@@ -86,6 +87,8 @@ def lib() -> ctypes.CDLL:
     L.lh_step.restype = ctypes.c_int
     L.lh_mh_step.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, i64, i64, i64, i64, ctypes.c_int, vp]
     L.lh_mh_step.restype = ctypes.c_int
+    L.lh_distill.argtypes = [vp, vp, vp, vp, i64, i64, i64, vp, vp, vp, vp, vp, vp]
+    L.lh_distill.restype = ctypes.c_int
     _lib = L
     return L
 
@@ -200,3 +203,29 @@ def mh_step(lam, R, h0, state, q, k, v, y, stream=None) -> None:
     _check(lib().lh_mh_step(lam.data_ptr(), R.data_ptr(), h0.data_ptr(), state.data_ptr(),
                             q.data_ptr(), k.data_ptr(), v.data_ptr(), y.data_ptr(), B, M, N, d,
                             io, _stream(q.device, stream)))
+
+
+def distill(A, theta, R, target, loss, dA, dtheta, dR, hhat=None, stream=None) -> None:
+    """Distillation objective (``lh_distill``): ``loss [D]`` and the gradients
+    ``dA, dtheta [D, d]`` (float32), ``dR [D, d]`` (complex64,
+    ``d/dRe R + i d/dIm R``) of the squared l2 error between the modal filter
+    of polar poles ``A e^{i theta}`` and residues ``R`` and ``target [D, L]``;
+    optionally the materialised filter ``hhat [D, L]``."""
+    import torch
+
+    D, d = A.shape
+    L = target.shape[1]
+    _need(A, "A", torch.float32, (D, d))
+    _need(theta, "theta", torch.float32, (D, d))
+    _need(R, "R", torch.complex64, (D, d))
+    _need(target, "target", torch.float32, (D, L))
+    _need(loss, "loss", torch.float32, (D,))
+    _need(dA, "dA", torch.float32, (D, d))
+    _need(dtheta, "dtheta", torch.float32, (D, d))
+    _need(dR, "dR", torch.complex64, (D, d))
+    if hhat is not None:
+        _need(hhat, "hhat", torch.float32, (D, L))
+    _check(lib().lh_distill(A.data_ptr(), theta.data_ptr(), R.data_ptr(), target.data_ptr(), D, d,
+                            L, loss.data_ptr(), dA.data_ptr(), dtheta.data_ptr(), dR.data_ptr(),
+                            hhat.data_ptr() if hhat is not None else None,
+                            _stream(A.device, stream)))

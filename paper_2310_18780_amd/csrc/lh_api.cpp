@@ -328,4 +328,48 @@ lh_status lh_mh_step(const lh_c32* lambda, const lh_c32* R, const float* h0, lh_
                     "multi-head step launch");
 }
 
+lh_status lh_distill(const float* A, const float* theta, const lh_c32* R, const float* target,
+                     int64_t D, int64_t d, int64_t L, float* loss, float* dA, float* dtheta,
+                     lh_c32* dR, float* hhat, void* stream)
+{
+    g_last_error[0] = '\0';
+    lh_status s;
+    if (!A || !theta || !R || !target || !loss || !dA || !dtheta || !dR)
+        return fail(LH_ERR_INVALID_ARG,
+                    "A, theta, R, target, loss, dA, dtheta and dR must not be NULL");
+    if (L < 1) return fail(LH_ERR_INVALID_ARG, "L = %lld must be >= 1", (long long)L);
+    if ((s = check_sizes(1, D, d, L)) != LH_OK) return s;
+    const Buf b_A = buf("A", A, sizeof(float) * D * d);
+    const Buf b_th = buf("theta", theta, sizeof(float) * D * d);
+    const Buf b_R = buf("R", R, sizeof(lh_c32) * D * d);
+    const Buf b_tg = buf("target", target, sizeof(float) * D * L);
+    const Buf b_loss = buf("loss", loss, sizeof(float) * D);
+    const Buf b_dA = buf("dA", dA, sizeof(float) * D * d);
+    const Buf b_dth = buf("dtheta", dtheta, sizeof(float) * D * d);
+    const Buf b_dR = buf("dR", dR, sizeof(lh_c32) * D * d);
+    const Buf b_h = buf("hhat", hhat, hhat ? sizeof(float) * D * L : 0);
+    if ((s = check_align(b_A, 4)) || (s = check_align(b_th, 4)) || (s = check_align(b_R, 8)) ||
+        (s = check_align(b_tg, 4)) || (s = check_align(b_loss, 4)) || (s = check_align(b_dA, 4)) ||
+        (s = check_align(b_dth, 4)) || (s = check_align(b_dR, 8)) || (s = check_align(b_h, 4)))
+        return s;
+    const Buf* ins[] = {&b_A, &b_th, &b_R, &b_tg};
+    const Buf* outs[] = {&b_loss, &b_dA, &b_dth, &b_dR, &b_h};
+    for (const Buf* o : outs) {
+        for (const Buf* i : ins)
+            if (overlaps(*o, *i)) return fail(LH_ERR_OVERLAP, "%s overlaps %s", o->name, i->name);
+        for (const Buf* o2 : outs)
+            if (o2 != o && overlaps(*o, *o2))
+                return fail(LH_ERR_OVERLAP, "%s overlaps %s", o->name, o2->name);
+    }
+    int dev = 0;
+    if ((s = check_device(&dev)) != LH_OK) return s;
+    const Buf* all[] = {&b_A, &b_th, &b_R, &b_tg, &b_loss, &b_dA, &b_dth, &b_dR, &b_h};
+    for (const Buf* b : all)
+        if ((s = check_accessible(*b, dev)) != LH_OK) return s;
+    return from_hip(lh::launch_distill(A, theta, reinterpret_cast<const float2*>(R), target, D,
+                                       d, L, loss, dA, dtheta, reinterpret_cast<float2*>(dR),
+                                       hhat, static_cast<hipStream_t>(stream)),
+                    "distillation launch");
+}
+
 }  // extern "C"

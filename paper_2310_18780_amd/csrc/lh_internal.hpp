@@ -68,6 +68,11 @@ hipError_t launch_step(const float2* lam, const float2* R, const float* h0, floa
                        const void* u_t, void* y_t, bool bf16_io, int64_t B, int64_t D,
                        int64_t d, bool aligned16, hipStream_t stream);
 
+// Distillation objective: loss and gradients per channel (targets [D, L]).
+hipError_t launch_distill(const float* A, const float* theta, const float2* R,
+                          const float* target, int64_t D, int64_t d, int64_t L, float* loss,
+                          float* dA, float* dtheta, float2* dR, float* hhat, hipStream_t stream);
+
 // Multi-head decode step (state [B, M, N, N, d]; q, k, v, y [B, M N]).
 hipError_t launch_mh_step(const float2* lam, const float2* R, const float* h0, float2* state,
                           const void* q, const void* k, const void* v, void* y, bool bf16_io,

@@ -21,9 +21,10 @@
 // and one contiguous kilobyte.  The entry loop is unrolled four times so that
 // every lane has four state loads in flight.  Each lane accumulates q_j times
 // its share of w[i,j] over all its entries; one reduction over the wave gives
-// y.  State stores are non-temporal (written once, not re-read here).  A
-// workgroup is four waves = four consecutive rows i of one (b, m), which share
-// their q and v loads through the cache.
+// y.  A workgroup is four waves = four consecutive rows i of one (b, m), which
+// share their q and v loads through the cache.  (Measured on the 256 MiB
+// bench state: non-temporal state stores, 2 or 8 rows per workgroup and
+// unrolling by 2 or 8 were all within 2%, none faster.)
 //
 // Generic path (any other d or alignment): a wavefront per row as well, one
 // entry per lane and a loop over the modes.
@@ -43,10 +44,10 @@ __device__ __forceinline__ float4 ld4(const float2* p)
     return make_float4(v.x, v.y, v.z, v.w);
 }
 
-__device__ __forceinline__ void st4_nt(float2* p, float4 a)
+__device__ __forceinline__ void st4(float2* p, float4 a)
 {
     const f4v v = {a.x, a.y, a.z, a.w};
-    __builtin_nontemporal_store(v, reinterpret_cast<f4v*>(p));
+    *reinterpret_cast<f4v*>(p) = v;
 }
 
 // sum over the 64 lanes of a wave, returned in every lane: DPP within rows of
@@ -121,7 +122,7 @@ __global__ __launch_bounds__(64 * kWaves) void mh_step_pairs_kernel(
             n4.w = fmaf(l4.z, x[s].w, l4.w * x[s].z);
             if (j < N) {
                 acc = fmaf(qj[s], w, acc);
-                st4_nt(xrow + int64_t(j) * d + 2 * p, n4);
+                st4(xrow + int64_t(j) * d + 2 * p, n4);
             }
         }
     }

@@ -211,3 +211,34 @@ def test_mh_step_reports_no_device_without_gpu():
     L = lh.lib()
     assert L.lh_mh_step(*mh_args()) == 4
     assert L.lh_mh_step(*mh_args(io=lh.LH_BF16, d=3)) == 4
+
+
+def distill_args(**kw):
+    a = dict(A=A, th=A + MB, R=A + 2 * MB, tg=A + 3 * MB, D=4, d=4, L=16, loss=A + 64 * MB,
+             dA=A + 65 * MB, dth=A + 66 * MB, dR=A + 67 * MB, h=None, stream=None)
+    a.update(kw)
+    return [a[k] for k in ("A", "th", "R", "tg", "D", "d", "L", "loss", "dA", "dth", "dR", "h",
+                           "stream")]
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(A=None), 1), (dict(th=None), 1), (dict(R=None), 1), (dict(tg=None), 1),
+    (dict(loss=None), 1), (dict(dA=None), 1), (dict(dth=None), 1), (dict(dR=None), 1),
+    (dict(D=0), 1), (dict(d=0), 1), (dict(d=1025), 1), (dict(L=0), 1),
+    (dict(D=1 << 40, L=1 << 30), 1),    # size overflow
+    (dict(dA=A + MB), 2),               # output overlaps theta
+    (dict(dth=A + 65 * MB + 4), 2),     # dtheta overlaps dA
+    (dict(h=A + 3 * MB + 16), 2),       # hhat overlaps the target
+    (dict(R=A + 2 * MB + 4), 1),        # misaligned complex64
+])
+def test_distill_rejects_bad_arguments(kw, status):
+    L = lh.lib()
+    assert L.lh_distill(*distill_args(**kw)) == status
+    assert L.lh_last_error().decode() != ""
+
+
+def test_distill_reports_no_device_without_gpu():
+    if not no_gpu():
+        pytest.skip("made-up addresses are only passed through when no GPU is visible")
+    assert lh.lib().lh_distill(*distill_args()) == 4
+    assert lh.lib().lh_distill(*distill_args(h=A + 128 * MB)) == 4

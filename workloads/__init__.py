@@ -51,6 +51,8 @@ __all__ = [
     "mh_workload",
     "mh_params",
     "mh_row",
+    "distill_params",
+    "distill_target",
 ]
 
 
@@ -246,3 +248,31 @@ def mh_row(w: MHWorkload, b: int) -> Tuple[np.ndarray, np.ndarray, np.ndarray]:
         a = rng.standard_normal((L, w.M * w.N), dtype=np.float32)
         out.append((bf16_round(a) if w.io == "bf16" else a).reshape(L, w.M, w.N))
     return out[0], out[1], out[2]
+
+
+# ----------------------------------------------------------------------------
+# distillation objective: modal parameters in polar form and target filters
+# ----------------------------------------------------------------------------
+
+def distill_params(w: Workload) -> Tuple[np.ndarray, np.ndarray, np.ndarray]:
+    """Starting point of a distillation: ``(A [D,d], theta [D,d], R [D,d])``,
+    the same draws as ``make_params`` (``A = r``, the pole's modulus, and
+    ``theta``) as float32 and complex64."""
+    rng = np.random.default_rng(w.seed)
+    r = rng.uniform(w.r_lo, w.r_hi, size=(w.D, w.d))
+    theta = rng.uniform(0.0, w.theta_hi, size=(w.D, w.d))
+    s = math.sqrt(w.r_var / 2.0)
+    re_r = rng.standard_normal((w.D, w.d)) * s
+    im_r = rng.standard_normal((w.D, w.d)) * s
+    return r.astype(np.float32), theta.astype(np.float32), (re_r + 1j * im_r).astype(np.complex64)
+
+
+def distill_target(w: Workload, L: int, tau: float = 512.0) -> np.ndarray:
+    """Synthetic real target filters ``[D, L]`` (``h_1 .. h_L``) standing in for
+    pre-trained long-convolution filters: unit normal draws under an
+    exponentially decaying envelope ``exp(-t / tau)``, from
+    ``default_rng([seed, 4])``."""
+    rng = np.random.default_rng([w.seed, 4])
+    g = rng.standard_normal((w.D, L), dtype=np.float32)
+    env = np.exp(-np.arange(1, L + 1, dtype=np.float64) / tau).astype(np.float32)
+    return (g * env[None, :]).astype(np.float32)
