@@ -50,6 +50,9 @@ def parse():
     p.add_argument("--multihead", action="store_true",
                    help="time the multi-head decode step (lh_mh_step) instead, on --mh-workload")
     p.add_argument("--mh-workload", default="mh")
+    p.add_argument("--distill", action="store_true",
+                   help="time the distillation objective (lh_distill) on --workload's filter "
+                        "bank with L = its T")
     return p.parse_args()
 
 
@@ -284,6 +287,91 @@ def multihead_main(args):
     print(json.dumps(out), flush=True)
 
 
+# declared flops of the distillation objective per (t, n): the running power
+# (complex product, 6), the filter term Re(R p) (2 FMA, 4); then the powers
+# again (6) and the two gradient sums e p and e (t-1) p (4 FMA, 8)
+DISTILL_FLOPS_PER_TAP_MODE = 24
+
+
+def distill_main(args):
+    import numpy as np
+    import torch
+
+    import paper_2310_18780_amd as lh
+    import workloads
+
+    lh.lib()
+    w = workloads.workload(args.workload)
+    L = w.T
+    A, th, R = workloads.distill_params(w)
+    tgt = workloads.distill_target(w, L)
+    tl = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()  # noqa: E731
+    At, tht, Rt, tg = tl(A), tl(th), tl(R), tl(tgt)
+    loss = torch.empty((w.D,), device="cuda")
+    dA = torch.empty((w.D, w.d), device="cuda")
+    dth = torch.empty_like(dA)
+    dR = torch.empty((w.D, w.d), dtype=torch.complex64, device="cuda")
+
+    def call():
+        lh.distill(At, tht, Rt, tg, loss, dA, dth, dR)
+
+    for _ in range(max(1, args.warmup)):
+        call()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    a, c = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    a.record(stream)
+    for _ in range(args.steps):
+        call()
+    c.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms = a.elapsed_time(c) / args.steps
+    flops = DISTILL_FLOPS_PER_TAP_MODE * w.D * L * w.d
+    tf = flops / (ms * 1e-3) / 1e12
+    nbytes = 4 * w.D * L + (4 + 4 + 8) * w.D * w.d * 2 + 4 * w.D
+    cpu = None
+    if not args.no_cpu_baseline:
+        import oracle
+        import oracle.distill as od
+
+        done, dt = 0, 0.0
+        while dt < 10.0 and done < w.D:
+            sl = slice(done, min(w.D, done + 16))
+            t1 = time.perf_counter()
+            od.distill_loss_grad(A[sl], th[sl], R[sl], tgt[sl])
+            dt += time.perf_counter() - t1
+            done = sl.stop
+        cpu = {"value": done * L / dt, "unit": "taps/s", "cores": oracle.native_threads(),
+               "kind": "oracle",
+               "sample": f"{done} of {w.D} channels (loss and gradients over L={L} taps, "
+                         f"d={w.d}, float64 numpy) in {dt:.2f} s",
+               "seconds": dt}
+    out = {
+        "metric": "distillation objective taps/s (loss + gradients, per channel and tap)",
+        "value": w.D * L / (ms * 1e-3),
+        "unit": "taps/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": wall * 1e3 / args.steps,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": f"distill_{w.name}", "D": w.D, "d": w.d, "L": L},
+        "ms_per_call": ms,
+        "roofline": {"bound": "alu", "achieved": tf, "peak": FP32_VALU_PEAK_TFLOPS,
+                     "unit": "TFLOP/s", "frac": tf / FP32_VALU_PEAK_TFLOPS, "traffic": None,
+                     "kernel": "distill_kernel", "flops_per_launch": flops,
+                     "bytes_per_launch": nbytes, "gbps": nbytes / (ms * 1e-3) / 1e9},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -296,6 +384,9 @@ def main():
         return
     if args.multihead:
         multihead_main(args)
+        return
+    if args.distill:
+        distill_main(args)
         return
 
     import torch
