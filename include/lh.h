@@ -140,6 +140,41 @@ lh_status lh_prefill(const lh_c32* lambda, const lh_c32* R, const float* h0,
                      int64_t chunk_len, void* workspace, size_t workspace_bytes,
                      void* stream);
 
+/* Longest prompt lh_prefill_fft accepts (transforms of at most 2^20 points). */
+#define LH_FFT_MAX_T (INT64_C(1) << 19)
+
+/*
+ * Workspace bytes lh_prefill_fft needs for these sizes; 0 when T == 0 and
+ * (size_t)-1 when the arguments are invalid or T > LH_FFT_MAX_T.  Pure
+ * function of its arguments.  About (2 + 2 ceil(B/2)) N D 4 bytes, with N the
+ * transform length below, plus partial states and small tables.
+ */
+size_t lh_prefill_fft_workspace_bytes(int64_t B, int64_t D, int64_t d, int64_t T);
+
+/*
+ * Prefill by FFT convolution (Sec. 3.4, fast pre-filling "via convolutions"):
+ * the same results as lh_prefill (outputs y[b,t,c] for t < T and state = x_T),
+ * computed the other way the paper describes:
+ *
+ *   hhat_0 = h0[c],  hhat_t = Re sum_n R[c,n] lambda[c,n]^(t-1)   (t < T; the
+ *       O(dT) evaluation of Lemma "ssmd_impulse")
+ *   y[b,t,c]     = sum_{j<=t} hhat_{t-j} u[b,j,c]   (eq. "cnn"), by N-point
+ *       FFTs with N the smallest power of two >= 2T - 1
+ *   state[b,c,n] = sum_{k<T} lambda[c,n]^(T-1-k) u[b,k,c]  (Vandermonde
+ *       contraction)
+ *
+ * Arguments, layouts, ownership and errors as lh_prefill (no chunk_len), with
+ *   T          : 0 <= T <= LH_FFT_MAX_T
+ *   workspace  : at least lh_prefill_fft_workspace_bytes(B,D,d,T) bytes,
+ *                256-byte aligned (NULL allowed when that size is 0)
+ * The rounding differs from the scan's (float32 transforms: an error near
+ * 1e-7 log2(N) of the largest outputs of a row, spread over the row).
+ */
+lh_status lh_prefill_fft(const lh_c32* lambda, const lh_c32* R, const float* h0,
+                         const void* u, int64_t B, int64_t D, int64_t d, int64_t T,
+                         lh_dtype io_dtype, lh_c32* state, void* y,
+                         void* workspace, size_t workspace_bytes, void* stream);
+
 /*
  * Decode step (Proposition "modal_realization"; App. B.1 for the real part):
  *   y_t[b,c]     = Re(sum_n R[c,n] state[b,c,n]) + h0[c] u_t[b,c]

@@ -6,6 +6,7 @@ calls the library.  Every step of the computation runs in the library's HIP
 kernels; there is no fallback.  PyTorch provides device memory and streams.
 
     prefill(lam, R, h0, u, state, y)   # y[b,t,c], t < T, and state = x_T
+    prefill_fft(lam, R, h0, u, state, y)  # the same results by FFT convolution
     step(lam, R, h0, state, u_t, y_t)  # y_t from x_t, then x_{t+1} in place
 
 ``lam``, ``R``: complex64 ``[D, d]``; ``h0``: float32 ``[D]``; ``u``, ``y``:
@@ -26,6 +27,8 @@ __all__ = [
     "library_path",
     "workspace_bytes",
     "prefill",
+    "fft_workspace_bytes",
+    "prefill_fft",
     "step",
     "mh_step",
     "distill",
@@ -83,6 +86,11 @@ def lib() -> ctypes.CDLL:
     L.lh_prefill.argtypes = [vp, vp, vp, vp, i64, i64, i64, i64, ctypes.c_int, vp, vp, i64, vp,
                              sz, vp]
     L.lh_prefill.restype = ctypes.c_int
+    L.lh_prefill_fft_workspace_bytes.argtypes = [i64, i64, i64, i64]
+    L.lh_prefill_fft_workspace_bytes.restype = sz
+    L.lh_prefill_fft.argtypes = [vp, vp, vp, vp, i64, i64, i64, i64, ctypes.c_int, vp, vp, vp, sz,
+                                 vp]
+    L.lh_prefill_fft.restype = ctypes.c_int
     L.lh_step.argtypes = [vp, vp, vp, vp, vp, vp, i64, i64, i64, ctypes.c_int, vp]
     L.lh_step.restype = ctypes.c_int
     L.lh_mh_step.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, i64, i64, i64, i64, ctypes.c_int, vp]
@@ -162,6 +170,37 @@ def prefill(lam, R, h0, u, state, y, workspace=None, chunk_len: int = 0, stream=
     _check(lib().lh_prefill(lam.data_ptr(), R.data_ptr(), h0.data_ptr(), u.data_ptr(), B, D, d, T,
                             io, state.data_ptr(), y.data_ptr(), chunk_len, ws_ptr, ws_len,
                             _stream(u.device, stream)))
+
+
+def fft_workspace_bytes(B: int, D: int, d: int, T: int) -> int:
+    n = lib().lh_prefill_fft_workspace_bytes(B, D, d, T)
+    if n == ctypes.c_size_t(-1).value:
+        raise LHError(1, f"invalid sizes for the FFT prefill B={B} D={D} d={d} T={T}")
+    return int(n)
+
+
+def prefill_fft(lam, R, h0, u, state, y, workspace=None, stream=None) -> None:
+    """``prefill``'s results by FFT convolution with the materialised filter
+    and a Vandermonde contraction for the state (``lh_prefill_fft``)."""
+    import torch
+
+    B, T, D = u.shape
+    d = lam.shape[1]
+    _need(lam, "lam", torch.complex64, (D, d))
+    _need(R, "R", torch.complex64, (D, d))
+    _need(h0, "h0", torch.float32, (D,))
+    _need(u, "u", u.dtype, (B, T, D))
+    _need(state, "state", torch.complex64, (B, D, d))
+    _need(y, "y", u.dtype, (B, T, D))
+    io = _io_dtype(u)
+    need = fft_workspace_bytes(B, D, d, T)
+    if need > 0 and workspace is None:
+        workspace = torch.empty(need, dtype=torch.uint8, device=u.device)
+    ws_ptr = workspace.data_ptr() if workspace is not None else None
+    ws_len = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    _check(lib().lh_prefill_fft(lam.data_ptr(), R.data_ptr(), h0.data_ptr(), u.data_ptr(), B, D,
+                                d, T, io, state.data_ptr(), y.data_ptr(), ws_ptr, ws_len,
+                                _stream(u.device, stream)))
 
 
 def step(lam, R, h0, state, u_t, y_t, stream=None) -> None:

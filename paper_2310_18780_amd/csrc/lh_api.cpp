@@ -10,6 +10,7 @@
 #include <string.h>
 
 #include "lh_internal.hpp"
+#include "prefill_fft.hpp"
 
 namespace {
 
@@ -128,6 +129,54 @@ lh_status from_hip(hipError_t e, const char* what)
     return fail(LH_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
 }
 
+// Buffer checks shared by both prefill entry points: alignment, workspace
+// size, overlaps, and that every buffer is accessible from the current device.
+lh_status check_prefill_buffers(const lh_c32* lambda, const lh_c32* R, const float* h0,
+                                const void* u, int64_t B, int64_t D, int64_t d, int64_t T,
+                                lh_dtype io_dtype, lh_c32* state, void* y, void* workspace,
+                                size_t ws_needed, size_t workspace_bytes)
+{
+    lh_status s;
+    const size_t es = io_dtype == LH_BF16 ? 2 : 4;
+    const size_t n_io = static_cast<size_t>(B) * T * D;
+    const Buf b_lam = buf("lambda", lambda, sizeof(lh_c32) * D * d);
+    const Buf b_R = buf("R", R, sizeof(lh_c32) * D * d);
+    const Buf b_h0 = buf("h0", h0, sizeof(float) * D);
+    const Buf b_u = buf("u", u, T > 0 ? es * n_io : 0);
+    const Buf b_state = buf("state", state, sizeof(lh_c32) * B * D * d);
+    const Buf b_y = buf("y", y, T > 0 ? es * n_io : 0);
+    const Buf b_ws = buf("workspace", workspace, ws_needed);
+
+    if ((s = check_align(b_lam, 8)) || (s = check_align(b_R, 8)) || (s = check_align(b_h0, 4)) ||
+        (s = check_align(b_state, 8)) || (s = check_align(b_u, es)) || (s = check_align(b_y, es)))
+        return s;
+    if (ws_needed > 0) {
+        if (!workspace)
+            return fail(LH_ERR_WORKSPACE, "workspace is NULL but %zu bytes are needed", ws_needed);
+        if (workspace_bytes < ws_needed)
+            return fail(LH_ERR_WORKSPACE, "workspace has %zu bytes, %zu are needed",
+                        workspace_bytes, ws_needed);
+        if ((s = check_align(b_ws, 256))) return s;
+    }
+    const Buf* ins[] = {&b_lam, &b_R, &b_h0, &b_u};
+    const Buf* outs[] = {&b_state, &b_y, &b_ws};
+    for (const Buf* o : outs) {
+        for (const Buf* i : ins)
+            if (overlaps(*o, *i))
+                return fail(LH_ERR_OVERLAP, "%s overlaps %s", o->name, i->name);
+        for (const Buf* o2 : outs)
+            if (o != o2 && overlaps(*o, *o2))
+                return fail(LH_ERR_OVERLAP, "%s overlaps %s", o->name, o2->name);
+    }
+
+    int dev = 0;
+    if ((s = check_device(&dev)) != LH_OK) return s;
+    const Buf* all[] = {&b_lam, &b_R, &b_h0, &b_u, &b_state, &b_y, &b_ws};
+    for (const Buf* b : all)
+        if ((s = check_accessible(*b, dev)) != LH_OK) return s;
+    return LH_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -182,44 +231,9 @@ lh_status lh_prefill(const lh_c32* lambda, const lh_c32* R, const float* h0, con
                              reinterpret_cast<uintptr_t>(y) % 16 != 0))
         return fail(LH_ERR_INVALID_ARG, "the matrix-core plan needs 16-byte aligned u and y");
 
-    const size_t es = io_dtype == LH_BF16 ? 2 : 4;
-    const size_t n_io = static_cast<size_t>(B) * T * D;
-    const Buf b_lam = buf("lambda", lambda, sizeof(lh_c32) * D * d);
-    const Buf b_R = buf("R", R, sizeof(lh_c32) * D * d);
-    const Buf b_h0 = buf("h0", h0, sizeof(float) * D);
-    const Buf b_u = buf("u", u, T > 0 ? es * n_io : 0);
-    const Buf b_state = buf("state", state, sizeof(lh_c32) * B * D * d);
-    const Buf b_y = buf("y", y, T > 0 ? es * n_io : 0);
-    const Buf b_ws = buf("workspace", workspace, plan.ws_bytes ? plan.ws_bytes : 0);
-
-    if ((s = check_align(b_lam, 8)) || (s = check_align(b_R, 8)) || (s = check_align(b_h0, 4)) ||
-        (s = check_align(b_state, 8)) || (s = check_align(b_u, es)) || (s = check_align(b_y, es)))
+    if ((s = check_prefill_buffers(lambda, R, h0, u, B, D, d, T, io_dtype, state, y, workspace,
+                                   plan.ws_bytes, workspace_bytes)) != LH_OK)
         return s;
-    if (plan.ws_bytes > 0) {
-        if (!workspace)
-            return fail(LH_ERR_WORKSPACE, "workspace is NULL but %zu bytes are needed",
-                        plan.ws_bytes);
-        if (workspace_bytes < plan.ws_bytes)
-            return fail(LH_ERR_WORKSPACE, "workspace has %zu bytes, %zu are needed",
-                        workspace_bytes, plan.ws_bytes);
-        if ((s = check_align(b_ws, 256))) return s;
-    }
-    const Buf* ins[] = {&b_lam, &b_R, &b_h0, &b_u};
-    const Buf* outs[] = {&b_state, &b_y, &b_ws};
-    for (const Buf* o : outs) {
-        for (const Buf* i : ins)
-            if (overlaps(*o, *i))
-                return fail(LH_ERR_OVERLAP, "%s overlaps %s", o->name, i->name);
-        for (const Buf* o2 : outs)
-            if (o != o2 && overlaps(*o, *o2))
-                return fail(LH_ERR_OVERLAP, "%s overlaps %s", o->name, o2->name);
-    }
-
-    int dev = 0;
-    if ((s = check_device(&dev)) != LH_OK) return s;
-    const Buf* all[] = {&b_lam, &b_R, &b_h0, &b_u, &b_state, &b_y, &b_ws};
-    for (const Buf* b : all)
-        if ((s = check_accessible(*b, dev)) != LH_OK) return s;
 
     return from_hip(
         lh::launch_prefill(reinterpret_cast<const float2*>(lambda),
@@ -227,6 +241,44 @@ lh_status lh_prefill(const lh_c32* lambda, const lh_c32* R, const float* h0, con
                            d, T, reinterpret_cast<float2*>(state), y, plan, workspace,
                            static_cast<hipStream_t>(stream)),
         "prefill launch");
+}
+
+size_t lh_prefill_fft_workspace_bytes(int64_t B, int64_t D, int64_t d, int64_t T)
+{
+    if (check_sizes(B, D, d, T) != LH_OK) return (size_t)-1;
+    lh::FftPlan p;
+    if (!lh::make_fft_plan(B, D, d, T, &p)) return (size_t)-1;
+    return p.ws_bytes;
+}
+
+lh_status lh_prefill_fft(const lh_c32* lambda, const lh_c32* R, const float* h0, const void* u,
+                         int64_t B, int64_t D, int64_t d, int64_t T, lh_dtype io_dtype,
+                         lh_c32* state, void* y, void* workspace, size_t workspace_bytes,
+                         void* stream)
+{
+    g_last_error[0] = '\0';
+    lh_status s;
+    if (!lambda || !R || !h0 || !state)
+        return fail(LH_ERR_INVALID_ARG, "lambda, R, h0 and state must not be NULL");
+    if ((s = check_sizes(B, D, d, T)) != LH_OK) return s;
+    if (T > LH_FFT_MAX_T)
+        return fail(LH_ERR_INVALID_ARG, "T = %lld exceeds LH_FFT_MAX_T = %lld", (long long)T,
+                    (long long)LH_FFT_MAX_T);
+    if (T > 0 && (!u || !y)) return fail(LH_ERR_INVALID_ARG, "u and y must not be NULL when T > 0");
+    if ((s = check_dtype(io_dtype)) != LH_OK) return s;
+    lh::FftPlan plan;
+    if (!lh::make_fft_plan(B, D, d, T, &plan))
+        return fail(LH_ERR_INVALID_ARG, "no FFT prefill plan for B=%lld D=%lld d=%lld T=%lld",
+                    (long long)B, (long long)D, (long long)d, (long long)T);
+    if ((s = check_prefill_buffers(lambda, R, h0, u, B, D, d, T, io_dtype, state, y, workspace,
+                                   plan.ws_bytes, workspace_bytes)) != LH_OK)
+        return s;
+    return from_hip(
+        lh::launch_prefill_fft(reinterpret_cast<const float2*>(lambda),
+                               reinterpret_cast<const float2*>(R), h0, u, io_dtype == LH_BF16, B,
+                               D, d, T, reinterpret_cast<float2*>(state), y, plan, workspace,
+                               static_cast<hipStream_t>(stream)),
+        "FFT prefill launch");
 }
 
 lh_status lh_step(const lh_c32* lambda, const lh_c32* R, const float* h0, lh_c32* state,

@@ -242,3 +242,73 @@ def test_distill_reports_no_device_without_gpu():
         pytest.skip("made-up addresses are only passed through when no GPU is visible")
     assert lh.lib().lh_distill(*distill_args()) == 4
     assert lh.lib().lh_distill(*distill_args(h=A + 128 * MB)) == 4
+
+
+def fft_ws(B, D, d, T):
+    """Workspace of the FFT prefill, from its documented layout: the N-point
+    twiddle table, per-mode polar constants, the filter spectrum and the
+    spectra of ceil(B/2) row pairs (N D complex64 each), each region rounded
+    up to 256 bytes; partial states of the state contraction come on top when
+    it splits time into several ranges."""
+    up = lambda x: -(-x // 256) * 256  # noqa: E731
+    N = 1
+    while N < 2 * T - 1:
+        N *= 2
+    return up(8 * N) + up(16 * D * d) + up(8 * N * D) + up(8 * ((B + 1) // 2) * N * D)
+
+
+def test_fft_workspace_sizes():
+    assert lh.fft_workspace_bytes(3, 8, 4, 0) == 0
+    for B, D, d, T in [(3, 10, 4, 100), (1, 1, 1, 1), (2, 7, 3, 2), (4, 33, 8, 256)]:
+        assert lh.fft_workspace_bytes(B, D, d, T) == fft_ws(B, D, d, T), (B, D, d, T)
+    # two 256-step ranges of the state contraction: partial states [2, B, D, d]
+    assert lh.fft_workspace_bytes(4, 33, 8, 257) == fft_ws(4, 33, 8, 257) + 2 * 4 * 33 * 8 * 8
+    # the long-prompt workload: 2^17-point transforms, 128 partial states
+    assert lh.fft_workspace_bytes(4, 1024, 32, 65536) == (
+        fft_ws(4, 1024, 32, 65536) + 128 * 4 * 1024 * 32 * 8)
+    L = lh.lib()
+    bad = ctypes.c_size_t(-1).value
+    max_t = 1 << 19
+    assert L.lh_prefill_fft_workspace_bytes(1, 4, 4, max_t) == fft_ws(1, 4, 4, max_t) + (
+        # 2048 ranges of 256 steps for 1 x 1 x 1 waves
+        2048 * 1 * 4 * 4 * 8)
+    for args in [(1, 4, 4, max_t + 1), (0, 4, 4, 8), (1, 0, 4, 8), (1, 4, 0, 8), (1, 4, 1025, 8),
+                 (1, 4, 4, -1), (1 << 40, 1 << 20, 64, 1 << 10)]:
+        assert L.lh_prefill_fft_workspace_bytes(*args) == bad, args
+
+
+def fft_args(**kw):
+    a = dict(lam=A, R=A + MB, h0=A + 2 * MB, u=A + 3 * MB, B=2, D=8, d=4, T=16, io=lh.LH_F32,
+             state=A + 64 * MB, y=A + 128 * MB, ws=A + 256 * MB, ws_bytes=1 << 20, stream=None)
+    a.update(kw)
+    return [a[k] for k in ("lam", "R", "h0", "u", "B", "D", "d", "T", "io", "state", "y", "ws",
+                           "ws_bytes", "stream")]
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(lam=None), 1), (dict(R=None), 1), (dict(h0=None), 1), (dict(state=None), 1),
+    (dict(u=None), 1), (dict(y=None), 1),
+    (dict(B=0), 1), (dict(D=-3), 1), (dict(d=0), 1), (dict(d=1025), 1), (dict(T=-1), 1),
+    (dict(T=(1 << 19) + 1), 1),          # longer than the transforms allow
+    (dict(io=7), 3),
+    (dict(u=A + 3 * MB + 2), 1),         # misaligned float32 input
+    (dict(y=A + 3 * MB + 64), 2),        # y overlaps u
+    (dict(state=A + MB + 8), 2),         # state overlaps R
+    (dict(ws=None), 5),                  # workspace needed
+    (dict(ws_bytes=16), 5),              # too small
+    (dict(ws=A + 256 * MB + 8), 1),      # misaligned workspace
+    (dict(ws=A + 128 * MB), 2),          # workspace overlaps y
+])
+def test_prefill_fft_rejects_bad_arguments(kw, status):
+    L = lh.lib()
+    assert L.lh_prefill_fft(*fft_args(**kw)) == status
+    assert L.lh_last_error().decode() != ""
+
+
+def test_prefill_fft_reports_no_device_without_gpu():
+    if not no_gpu():
+        pytest.skip("made-up addresses are only passed through when no GPU is visible")
+    L = lh.lib()
+    assert L.lh_prefill_fft(*fft_args()) == 4
+    assert L.lh_prefill_fft(*fft_args(io=lh.LH_BF16, B=3, d=7)) == 4
+    assert L.lh_prefill_fft(*fft_args(T=0, u=None, y=None, ws=None, ws_bytes=0)) == 4

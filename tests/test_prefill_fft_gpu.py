@@ -1,0 +1,209 @@
+"""GPU parity of the FFT prefill (``lh_prefill_fft``) against the CPU oracle on
+the same seeded inputs: outputs by direct causal convolution with the
+materialised filter, states by direct Vandermonde sums.
+
+Tolerances are those of the scan prefill (``parity_util``): per (b, c) row
+``max_t |y_gpu - y_ref| <= 1e-4 max_t |y_ref|`` (float32), bfloat16 outputs
+within one rounding of that, states ``max_n |x_gpu - x_ref| <= 1e-4
+max_n |x_ref|``.  A float32 transform of N points carries an error near
+1e-7 log2(N) of the row's largest outputs, spread evenly over the row, so the
+row-relative bound holds with margin for every N allowed (N <= 2^20).
+"""
+from __future__ import annotations
+
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+import workloads
+from parity_util import (_np, check_x, check_y, compare_full, compare_rows, sample_rows,
+                         to_device)
+
+pytestmark = pytest.mark.gpu
+
+
+def _log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    import torch
+
+    import paper_2310_18780_amd as lh
+
+    assert torch.cuda.is_available(), "GPU tests need a HIP device"
+    lh.lib()
+    yield
+
+
+def run_fft(t):
+    """FFT prefill then the decode steps of ``t['ud']`` (as ``parity_util.run_gpu``)."""
+    import torch
+
+    import paper_2310_18780_amd as lh
+
+    B, T, D = t["u"].shape
+    K = t["ud"].shape[0]
+    d = t["lam"].shape[1]
+    dev = t["u"].device
+    y = torch.full((B, T, D), float("nan"), dtype=t["u"].dtype, device=dev)
+    state = torch.full((B, D, d), complex(float("nan"), float("nan")), dtype=torch.complex64,
+                       device=dev)
+    lh.prefill_fft(t["lam"], t["R"], t["h0"], t["u"], state, y)
+    x_T = state.clone()
+    y_dec = torch.full((K, B, D), float("nan"), dtype=t["u"].dtype, device=dev)
+    for k in range(K):
+        lh.step(t["lam"], t["R"], t["h0"], state, t["ud"][k], y_dec[k])
+    torch.cuda.synchronize()
+    return dict(y_prefill=y, x_T=x_T, y_dec=y_dec, x_end=state)
+
+
+def inputs(B, D, d, T, K, io, seed=0, r=(0.5, 0.999), theta=np.pi):
+    w = workloads.Workload("case", B, D, d, T, K, io, r[0], r[1], theta, 1.0 / d, seed)
+    return w, workloads.make_inputs(w)
+
+
+# (B, D, d, T, K, io)
+SMALL = [
+    (1, 4, 4, 64, 4, "f32"),       # the tiny workload's shape: N = 128 (16 x 8)
+    (2, 70, 16, 300, 5, "f32"),    # N = 1024, D not a multiple of the 32-channel groups
+    (3, 130, 3, 257, 4, "bf16"),   # odd B (last pair half empty), odd d, bfloat16
+    (1, 7, 1, 100, 3, "f32"),      # d = 1
+    (2, 10, 4, 1, 3, "f32"),       # T = 1: N = 1
+    (1, 8, 4, 2, 3, "f32"),        # T = 2: N = 4 (2 x 2)
+    (3, 9, 2, 3, 2, "bf16"),       # T = 3: N = 8 (4 x 2), bfloat16
+    (2, 10, 4, 0, 3, "f32"),       # T = 0: zero state, y untouched
+    (5, 33, 64, 129, 3, "f32"),    # two groups of 4 mode chunks, two row groups
+    (2, 16, 17, 1000, 3, "f32"),   # ragged last mode chunk, 4 ranges of the state sum
+    (1, 9, 100, 40, 2, "f32"),     # d = 100: 13 mode chunks
+    (4, 64, 32, 4096, 3, "f32"),   # N = 8192 (128 x 64)
+    (2, 40, 16, 2049, 3, "bf16"),  # T just past a power of two: N = 8192
+    (6, 24, 8, 513, 2, "f32"),     # three pairs
+]
+
+
+@pytest.mark.parametrize("case", SMALL, ids=[
+    f"B{c[0]}_D{c[1]}_d{c[2]}_T{c[3]}_K{c[4]}_{c[5]}" for c in SMALL])
+def test_small_case(case):
+    B, D, d, T, K, io = case
+    _log(f"[fft small] {case}")
+    w, (lam, R, h0, up, ud) = inputs(B, D, d, T, K, io)
+    ref = oracle.run(lam, R, h0, up, ud)
+    out = run_fft(to_device(lam, R, h0, up, ud, io))
+    _log(f"[fft small] {case} max row-relative errors {compare_full(out, ref, io)}")
+
+
+def test_t0_leaves_outputs_untouched():
+    import torch
+
+    import paper_2310_18780_amd as lh
+
+    w, (lam, R, h0, up, ud) = inputs(2, 10, 4, 0, 1, "f32")
+    t = to_device(lam, R, h0, up, ud, "f32")
+    state = torch.full((2, 10, 4), complex(1.0, 2.0), dtype=torch.complex64, device="cuda")
+    y = torch.empty((2, 0, 10), device="cuda")
+    lh.prefill_fft(t["lam"], t["R"], t["h0"], t["u"], state, y)
+    torch.cuda.synchronize()
+    assert torch.count_nonzero(state).item() == 0
+
+
+@pytest.mark.parametrize("name", ["c5", "c3"])
+def test_full_workload_sampled_rows(name):
+    """Full-size workload through the FFT prefill: every output and state of
+    sampled (b, c) rows against the oracle."""
+    import torch
+
+    w = workloads.workload(name).with_(K=2)
+    _log(f"[fft full] {w}")
+    lam, R, h0, up, ud = workloads.make_inputs(w)
+    t = to_device(lam, R, h0, up, ud, w.io)
+    out = run_fft(t)
+    rows = sample_rows(w.B, w.D, 12)
+    bs = torch.tensor([b for b, _ in rows], device="cuda")
+    cs = torch.tensor([c for _, c in rows], device="cuda")
+    got = dict(y_prefill=_np(out["y_prefill"][bs, :, cs]),
+               y_dec=_np(out["y_dec"][:, bs, cs].T.contiguous()),
+               x_T=_np(out["x_T"][bs, cs]), x_end=_np(out["x_end"][bs, cs]))
+    del out, t
+    torch.cuda.empty_cache()
+    ref = oracle.run_rows(lam, R, h0, up, ud, rows)
+    _log(f"[fft full] {name} rows={len(rows)} errors {compare_rows(got, ref, w.io)}")
+
+
+@pytest.mark.parametrize("T", [70000, 1 << 19])
+def test_long_prompts_sampled_outputs(T):
+    """Transforms of 2^18 points (512 x 512, 16-channel groups in every pass)
+    and of the largest size, 2^20 points (1024 x 1024, 8-channel groups):
+    sampled outputs one by one and the states of sampled rows."""
+    import torch
+
+    import paper_2310_18780_amd as lh
+
+    B, D, d = 3, 20, 8
+    w, (lam, R, h0, up, ud) = inputs(B, D, d, T, 0, "f32", r=(0.99, 0.99999))
+    _log(f"[fft long] T={T}")
+    t = to_device(lam, R, h0, up, ud, "f32")
+    y = torch.empty((B, T, D), device="cuda")
+    state = torch.empty((B, D, d), dtype=torch.complex64, device="cuda")
+    lh.prefill_fft(t["lam"], t["R"], t["h0"], t["u"], state, y)
+    torch.cuda.synchronize()
+    yg = y.cpu().numpy()
+    xg = state.cpu().numpy()
+    rng = np.random.default_rng(5)
+    rows = sample_rows(B, D, 6)
+    for b, c in rows:
+        h = oracle.filter_taps(lam[c:c + 1], R[c:c + 1], h0[c:c + 1], T)[0]
+        u = up[b, :, c].astype(np.float64)
+        ts = sorted({0, 1, T - 1, *rng.integers(T, size=40).tolist()})
+        ref = np.array([oracle.conv_at(h, u, int(tt)) for tt in ts])
+        got = yg[b, ts, c]
+        # the bound uses the largest sampled output (at most the row maximum)
+        check_y(got[None], ref[None], "f32", f"long prompt y (b={b}, c={c})")
+        xr = oracle.state_after(lam[c].astype(np.complex128), u, T)
+        check_x(xg[b, c][None], xr[None], f"long prompt state (b={b}, c={c})")
+
+
+def test_agrees_with_scan_prefill_on_long_prompt():
+    """The two prefills of the library give the same results within the
+    tolerance on the long-prompt workload (GPU against GPU, all rows)."""
+    import torch
+
+    import paper_2310_18780_amd as lh
+
+    w = workloads.workload("c5").with_(K=0)
+    lam, R, h0, up, ud = workloads.make_inputs(w)
+    t = to_device(lam, R, h0, up, ud, w.io)
+    y1 = torch.empty_like(t["u"])
+    y2 = torch.empty_like(t["u"])
+    s1 = torch.empty((w.B, w.D, w.d), dtype=torch.complex64, device="cuda")
+    s2 = torch.empty_like(s1)
+    lh.prefill(t["lam"], t["R"], t["h0"], t["u"], s1, y1)
+    lh.prefill_fft(t["lam"], t["R"], t["h0"], t["u"], s2, y2)
+    torch.cuda.synchronize()
+    d1 = (y1 - y2).abs().amax(dim=1)          # [B, D]
+    m1 = y1.abs().amax(dim=1)
+    assert bool(torch.all(d1 <= 2e-4 * m1)), float((d1 / m1).max())
+    e = (s1 - s2).abs().amax(dim=2)
+    m = s1.abs().amax(dim=2)
+    assert bool(torch.all(e <= 2e-4 * m)), float((e / m).max())
+
+
+def test_bitwise_determinism():
+    import torch
+
+    import paper_2310_18780_amd as lh
+
+    w, (lam, R, h0, up, ud) = inputs(3, 48, 16, 3000, 0, "f32", seed=4)
+    t = to_device(lam, R, h0, up, ud, "f32")
+    res = []
+    for _ in range(2):
+        y = torch.empty_like(t["u"])
+        s = torch.empty((3, 48, 16), dtype=torch.complex64, device="cuda")
+        lh.prefill_fft(t["lam"], t["R"], t["h0"], t["u"], s, y)
+        torch.cuda.synchronize()
+        res.append((y.cpu().numpy(), s.cpu().numpy()))
+    assert np.array_equal(res[0][0].view(np.uint32), res[1][0].view(np.uint32))
+    assert np.array_equal(res[0][1].view(np.uint64), res[1][1].view(np.uint64))
