@@ -50,6 +50,10 @@ def parse():
     p.add_argument("--multihead", action="store_true",
                    help="time the multi-head decode step (lh_mh_step) instead, on --mh-workload")
     p.add_argument("--mh-workload", default="mh")
+    p.add_argument("--fft", action="store_true",
+                   help="time the FFT prefill (lh_prefill_fft) beside the scan prefill on "
+                        "--fft-workload")
+    p.add_argument("--fft-workload", default="c5")
     p.add_argument("--distill", action="store_true",
                    help="time the distillation objective (lh_distill) on --workload's filter "
                         "bank with L = its T")
@@ -372,6 +376,125 @@ def distill_main(args):
     print(json.dumps(out), flush=True)
 
 
+def fft_pass_bytes(w):
+    """HBM bytes the FFT prefill's passes move by design (each pass reads and
+    writes its arrays once): filter [T, D] written and read, its spectrum
+    written by the column pass and read and written by the row pass, the input
+    pairs' spectra written, read and written in the row pass and read by the
+    inverse column pass, the spectrum read once per pair, u read twice (the
+    transform and the state contraction), y and the state written."""
+    es = 2 if w.io == "bf16" else 4
+    N = 1
+    while N < 2 * w.T - 1:
+        N *= 2
+    npair = (w.B + 1) // 2
+    spec = 8 * N * w.D
+    return (2 * 4 * w.T * w.D + 3 * spec + 4 * npair * spec + npair * spec
+            + 2 * es * w.B * w.T * w.D + es * w.B * w.T * w.D + 8 * w.B * w.D * w.d)
+
+
+def fft_cpu_baseline(w, seconds=12.0):
+    """The oracle (direct float64 convolution and Vandermonde sums) on complete
+    prompt rows of the workload, about ``seconds`` of work."""
+    import numpy as np
+
+    import oracle
+    import workloads
+
+    lam, R, h0 = workloads.make_params(w)
+    rate = 0.5e9 * max(1, oracle.native_threads())
+    rows_wanted = int(max(8, min(w.B * w.D, seconds * rate / (w.T * w.T / 2))))
+    up = np.empty((1, w.T, w.D), np.float32)
+    up[0] = workloads.prompt_row(w, 0)
+    ud = np.empty((1, 0, w.D), np.float32)
+    rows = [(0, c) for c in range(min(rows_wanted, w.D))]
+    t0 = time.perf_counter()
+    oracle.run_rows(lam, R, h0, up, ud, rows)
+    dt = time.perf_counter() - t0
+    return {"value": len(rows) / w.D * w.T / dt, "unit": "tokens/s",
+            "cores": oracle.native_threads(), "kind": "oracle",
+            "sample": (f"{len(rows)} (b,c) rows of {w.name} (T={w.T} prompt outputs by direct "
+                       f"float64 convolution and the state by direct sums) in {dt:.2f} s; value "
+                       f"= prompt tokens per second scaled to whole sequences (rows / D * T / "
+                       f"time)"),
+            "seconds": dt}
+
+
+def fft_main(args):
+    import torch
+
+    import paper_2310_18780_amd as lh
+    import workloads
+
+    lh.lib()
+    w = workloads.workload(args.fft_workload).with_(K=1)
+    t = make_device_inputs(w)
+    B, T, D, d = w.B, w.T, w.D, w.d
+    state = torch.empty((B, D, d), dtype=torch.complex64, device="cuda")
+    y = torch.empty_like(t["u"])
+    wsf = lh.fft_workspace_bytes(B, D, d, T)
+    ws_fft = torch.empty(max(wsf, 1), dtype=torch.uint8, device="cuda")
+    wss = lh.workspace_bytes(B, D, d, T)
+    ws_scan = torch.empty(max(wss, 1), dtype=torch.uint8, device="cuda")
+    stream = torch.cuda.current_stream()
+
+    def fft():
+        lh.prefill_fft(t["lam"], t["R"], t["h0"], t["u"], state, y, workspace=ws_fft)
+
+    def scan():
+        lh.prefill(t["lam"], t["R"], t["h0"], t["u"], state, y, workspace=ws_scan)
+
+    def timed(fn):
+        for _ in range(max(1, args.warmup)):
+            fn()
+        torch.cuda.synchronize()
+        marks = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                 for _ in range(args.steps)]
+        t0 = time.perf_counter()
+        for a, c in marks:
+            a.record(stream)
+            fn()
+            c.record(stream)
+        torch.cuda.synchronize()
+        wall = (time.perf_counter() - t0) * 1e3 / args.steps
+        ms = sorted(a.elapsed_time(c) for a, c in marks)
+        return ms[len(ms) // 2], wall
+
+    fft_ms, fft_wall = timed(fft)
+    scan_ms, _ = timed(scan)
+    alg = prefill_bytes(w)
+    gbs = alg / (fft_ms * 1e-3) / 1e9
+    pbytes = fft_pass_bytes(w)
+    cpu = None if args.no_cpu_baseline else fft_cpu_baseline(w)
+    out = {
+        "metric": "prefill tokens/s (FFT convolution prefill)",
+        "value": B * T / (fft_ms * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": fft_wall,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": f"fft_prefill_{w.name}", "B": B, "D": D, "d": d, "T": T,
+                   "io": w.io, "workspace_bytes": wsf},
+        "prefill_ms": fft_ms,
+        "scan_prefill_ms": scan_ms,
+        "scan_prefill_tokens_per_s": B * T / (scan_ms * 1e-3),
+        "fft_over_scan_time": fft_ms / scan_ms,
+        "roofline": {"bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": gbs / HBM_PEAK_GBS, "traffic": None,
+                     "kernel": "lh_prefill_fft (all passes)", "bytes_per_launch": alg,
+                     "pass_bytes_per_launch": pbytes,
+                     "pass_gbps": pbytes / (fft_ms * 1e-3) / 1e9},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -387,6 +510,9 @@ def main():
         return
     if args.distill:
         distill_main(args)
+        return
+    if args.fft:
+        fft_main(args)
         return
 
     import torch

@@ -24,11 +24,15 @@
 // The filter spectrum comes from the same passes A and B (forward only).
 // Every pass keeps the channel index fastest in memory, as u and y have it:
 // a workgroup transforms CW adjacent channels, so each global access is a
-// contiguous run of CW values, and the transform itself runs in LDS
-// (in-place radix-2 stages fused in pairs into 4-point butterflies;
-// decimation in time from bit-reversed rows, decimation in frequency into
-// bit-reversed rows, so no reordering pass is needed).  Twiddles come from
-// one N-point table computed in float64 and rounded once.
+// contiguous run of CW values.  The transform runs on a tile in LDS as
+// Stockham autosort stages (natural order in and out, so no reordering pass):
+// radix-8 butterflies in registers, one radix-2 or radix-4 stage for the
+// remaining factor, one barrier between the reads and the writes of a stage.
+// Transform lengths are template parameters, so every loop over a thread's
+// elements is unrolled and all of a tile's global loads are in flight
+// together (the row pass also loads its slice of the filter spectrum up
+// front).  Twiddles come from one N-point table computed in float64 and
+// rounded once; a butterfly loads its base twiddle and forms the powers.
 //
 // The filter is evaluated per thread over 64 consecutive steps from a start
 // power in polar form (log2 |lambda| and the angle reduction in float64, then
@@ -46,6 +50,7 @@ constexpr int kHSeg = 64;         // filter steps per thread
 constexpr int kSSeg = 256;        // state contraction: steps between polar restarts
 constexpr int kSM = 8;            // state contraction: modes per lane
 constexpr int kSR = 4;            // state contraction: batch rows per lane
+constexpr int kPf = 8;            // state contraction: steps per prefetched block
 constexpr int kStateWaves = 8192; // state contraction: waves to aim for (8 per SIMD)
 
 __device__ __forceinline__ float2 cadd(float2 a, float2 b) { return make_float2(a.x + b.x, a.y + b.y); }
@@ -70,110 +75,127 @@ __device__ __forceinline__ float2 quarter(float2 t)
     return INV ? make_float2(-t.y, t.x) : make_float2(t.y, -t.x);
 }
 
-__device__ __forceinline__ int brev(int x, int bits)
+// Transform tile of L = 2^LOGL points for CW adjacent channels, in LDS as
+// x[row * CW + ch] (64 KiB at most); every thread holds EPT elements.
+template <int LOGL>
+struct Tile {
+    static constexpr int L = 1 << LOGL;
+    static constexpr int CW = L * 32 <= kLdsElems ? 32 : L * 16 <= kLdsElems ? 16 : 8;
+    static constexpr int E = L * CW;
+    static constexpr int EPT = (E + kThreads - 1) / kThreads;
+};
+
+constexpr int ilog2(int x) { return x <= 1 ? 0 : 1 + ilog2(x / 2); }
+
+// DFT of R = 2, 4 or 8 points in registers (forward: omega_R = e^{-2 pi i / R})
+template <bool INV>
+__device__ __forceinline__ void dft4(float2& a, float2& b, float2& c, float2& d)
 {
-    return bits == 0 ? 0 : static_cast<int>(__builtin_bitreverse32(static_cast<uint32_t>(x)) >> (32 - bits));
+    const float2 t0 = cadd(a, c), t1 = csub(a, c), t2 = cadd(b, d);
+    const float2 t3 = quarter<INV>(csub(b, d));
+    a = cadd(t0, t2);
+    c = csub(t0, t2);
+    b = cadd(t1, t3);
+    d = csub(t1, t3);
 }
 
-// In-place FFT of L = 2^logL points of CW interleaved sequences in LDS
-// (x[row * CW + ch]): decimation in time, rows in bit-reversed order on entry
-// and in natural order on exit.  Radix-2 stages of sizes m1 and 2 m1 are
-// fused into one 4-point butterfly (a single radix-2 stage first when logL is
-// odd); every fused pass ends with a barrier.  tw is the N-point table
-// (N = 2^logN >= L).
-template <int CW, bool INV>
-__device__ void fft_dit(float2* x, int logL, const float2* __restrict__ tw, int logN)
+template <int R, bool INV>
+__device__ __forceinline__ void dft(float2 (&v)[R])
 {
-    const int L = 1 << logL;
-    int s = 1;
-    if (logL & 1) {
-        for (int q = threadIdx.x; q < (L >> 1) * CW; q += kThreads) {
-            const int ch = q % CW, k = q / CW;
-            float2* p = x + 2 * k * CW + ch;
-            const float2 a = p[0], b = p[CW];
-            p[0] = cadd(a, b);
-            p[CW] = csub(a, b);
-        }
-        __syncthreads();
-        s = 2;
-    }
-    for (; s < logL; s += 2) {
-        const int m1 = 1 << s, h1 = m1 >> 1;
-        for (int q = threadIdx.x; q < (L >> 2) * CW; q += kThreads) {
-            const int ch = q % CW, tq = q / CW;
-            const int g = tq >> (s - 1), j = tq & (h1 - 1);
-            float2* p = x + (2 * g * m1 + j) * CW + ch;
-            float2 x0 = p[0], x1 = p[h1 * CW], x2 = p[m1 * CW], x3 = p[(m1 + h1) * CW];
-            const float2 w1 = twiddle<INV>(tw, int64_t(j) << (logN - s));      // omega_m1^j
-            const float2 w2 = twiddle<INV>(tw, int64_t(j) << (logN - s - 1));  // omega_2m1^j
-            float2 t = cmul(w1, x1);
-            x1 = csub(x0, t);
-            x0 = cadd(x0, t);
-            t = cmul(w1, x3);
-            x3 = csub(x2, t);
-            x2 = cadd(x2, t);
-            t = cmul(w2, x2);
-            x2 = csub(x0, t);
-            x0 = cadd(x0, t);
-            t = quarter<INV>(cmul(w2, x3));  // omega_2m1^(j + m1/2)
-            x3 = csub(x1, t);
-            x1 = cadd(x1, t);
-            p[0] = x0;
-            p[h1 * CW] = x1;
-            p[m1 * CW] = x2;
-            p[(m1 + h1) * CW] = x3;
-        }
-        __syncthreads();
+    if constexpr (R == 2) {
+        const float2 a = v[0];
+        v[0] = cadd(a, v[1]);
+        v[1] = csub(a, v[1]);
+    } else if constexpr (R == 4) {
+        dft4<INV>(v[0], v[1], v[2], v[3]);
+    } else {
+        static_assert(R == 8, "radix 2, 4 or 8");
+        float2 e0 = v[0], e1 = v[2], e2 = v[4], e3 = v[6];
+        float2 o0 = v[1], o1 = v[3], o2 = v[5], o3 = v[7];
+        dft4<INV>(e0, e1, e2, e3);
+        dft4<INV>(o0, o1, o2, o3);
+        const float h = 0.70710678118654752440f;  // omega_8 = (1 -+ i) / sqrt 2
+        o1 = INV ? make_float2(h * (o1.x - o1.y), h * (o1.x + o1.y))
+                 : make_float2(h * (o1.x + o1.y), h * (o1.y - o1.x));
+        o2 = quarter<INV>(o2);
+        o3 = INV ? make_float2(-h * (o3.x + o3.y), h * (o3.x - o3.y))
+                 : make_float2(h * (o3.y - o3.x), -h * (o3.x + o3.y));
+        v[0] = cadd(e0, o0);
+        v[4] = csub(e0, o0);
+        v[1] = cadd(e1, o1);
+        v[5] = csub(e1, o1);
+        v[2] = cadd(e2, o2);
+        v[6] = csub(e2, o2);
+        v[3] = cadd(e3, o3);
+        v[7] = csub(e3, o3);
     }
 }
 
-// The same transform by decimation in frequency: rows in natural order on
-// entry, bit-reversed on exit.  The caller has synchronised the buffer.
-template <int CW, bool INV>
-__device__ void fft_dif(float2* x, int logL, const float2* __restrict__ tw, int logN)
+// One Stockham autosort stage of radix R after NS points have been combined:
+// butterfly j reads x[j + r L/R], multiplies by omega_(NS R)^((j mod NS) r),
+// transforms, and writes x[(j / NS) NS R + (j mod NS) + r NS].  All reads
+// happen before a barrier, all writes after it, so one buffer serves.
+template <int LOGL, int R, int NS, bool INV>
+__device__ __forceinline__ void stage(float2* xs, const float2* __restrict__ tw, int logN)
 {
-    const int L = 1 << logL;
-    int s = logL;
-    for (; s >= 2; s -= 2) {
-        const int m1 = 1 << (s - 1), h1 = m1 >> 1;
-        for (int q = threadIdx.x; q < (L >> 2) * CW; q += kThreads) {
-            const int ch = q % CW, tq = q / CW;
-            const int g = tq >> (s - 2), j = tq & (h1 - 1);
-            float2* p = x + (2 * g * m1 + j) * CW + ch;
-            float2 x0 = p[0], x1 = p[h1 * CW], x2 = p[m1 * CW], x3 = p[(m1 + h1) * CW];
-            const float2 w2 = twiddle<INV>(tw, int64_t(j) << (logN - s));      // omega_2m1^j
-            const float2 w1 = twiddle<INV>(tw, int64_t(j) << (logN - s + 1));  // omega_m1^j
-            float2 a = cadd(x0, x2), b = cmul(csub(x0, x2), w2);
-            x0 = a;
-            x2 = b;
-            a = cadd(x1, x3);
-            b = quarter<INV>(cmul(csub(x1, x3), w2));
-            x1 = a;
-            x3 = b;
-            a = cadd(x0, x1);
-            b = cmul(csub(x0, x1), w1);
-            x0 = a;
-            x1 = b;
-            a = cadd(x2, x3);
-            b = cmul(csub(x2, x3), w1);
-            x2 = a;
-            x3 = b;
-            p[0] = x0;
-            p[h1 * CW] = x1;
-            p[m1 * CW] = x2;
-            p[(m1 + h1) * CW] = x3;
+    constexpr int L = Tile<LOGL>::L, CW = Tile<LOGL>::CW;
+    constexpr int NB = (L / R) * CW;
+    constexpr int BPT = (NB + kThreads - 1) / kThreads;
+    constexpr int kShift = ilog2(NS * R);
+    float2 v[BPT][R];
+    float2 w[BPT];
+#pragma unroll
+    for (int b = 0; b < BPT; ++b) {
+        const int q = threadIdx.x + b * kThreads;
+        if (NB % kThreads == 0 || q < NB) {
+            const int ch = q % CW, j = q / CW;
+#pragma unroll
+            for (int r = 0; r < R; ++r) v[b][r] = xs[(j + r * (L / R)) * CW + ch];
+            if (NS > 1) w[b] = twiddle<INV>(tw, int64_t(j % NS) << (logN - kShift));
         }
-        __syncthreads();
     }
-    if (s == 1) {
-        for (int q = threadIdx.x; q < (L >> 1) * CW; q += kThreads) {
-            const int ch = q % CW, k = q / CW;
-            float2* p = x + 2 * k * CW + ch;
-            const float2 a = p[0], b = p[CW];
-            p[0] = cadd(a, b);
-            p[CW] = csub(a, b);
+    __syncthreads();
+#pragma unroll
+    for (int b = 0; b < BPT; ++b) {
+        const int q = threadIdx.x + b * kThreads;
+        if (NB % kThreads == 0 || q < NB) {
+            const int ch = q % CW, j = q / CW;
+            if (NS > 1) {
+                float2 wr = w[b];
+#pragma unroll
+                for (int r = 1; r < R; ++r) {
+                    v[b][r] = cmul(v[b][r], wr);
+                    if (r + 1 < R) wr = cmul(wr, w[b]);
+                }
+            }
+            dft<R, INV>(v[b]);
+            const int base = (j / NS) * NS * R + j % NS;
+#pragma unroll
+            for (int r = 0; r < R; ++r) xs[(base + r * NS) * CW + ch] = v[b][r];
         }
-        __syncthreads();
+    }
+    __syncthreads();
+}
+
+template <int LOGL, int NS, bool INV>
+__device__ __forceinline__ void stages8(float2* xs, const float2* __restrict__ tw, int logN)
+{
+    if constexpr (NS < (1 << LOGL)) {
+        stage<LOGL, 8, NS, INV>(xs, tw, logN);
+        stages8<LOGL, NS * 8, INV>(xs, tw, logN);
+    }
+}
+
+// In-place transform of the tile (natural order in and out): one stage of
+// radix 2^(LOGL mod 3) (or 8) followed by radix-8 stages.  The caller has
+// synchronised the buffer; it is synchronised on return.
+template <int LOGL, bool INV>
+__device__ __forceinline__ void fft_tile(float2* xs, const float2* __restrict__ tw, int logN)
+{
+    if constexpr (LOGL > 0) {
+        constexpr int R0 = LOGL % 3 == 0 ? 8 : 1 << (LOGL % 3);
+        stage<LOGL, R0, 1, INV>(xs, tw, logN);
+        stages8<LOGL, R0, INV>(xs, tw, logN);
     }
 }
 
@@ -246,135 +268,185 @@ __global__ __launch_bounds__(kThreads) void fft_filter_kernel(const float2* __re
 
 // ------------------------------------------------------------ pass A
 // Forward column transforms of the real input pairs (or of the filter, with
-// B = 1): workgroup = (CW channels, column n1, pair p).
-template <typename IO, int CW>
+// B = 1): workgroup = (CW channels, column n1, pair p); N2 = 2^LOGL.
+template <typename IO, int LOGL>
 __global__ __launch_bounds__(kThreads) void fft_cols_fwd_kernel(const IO* __restrict__ u,
                                                                 int64_t B, int64_t T, int64_t D,
-                                                                int logN1, int logN2,
+                                                                int logN1,
                                                                 const float2* __restrict__ tw,
                                                                 float2* __restrict__ Z)
 {
-    extern __shared__ float2 xs[];  // [N2][CW]
-    const int logN = logN1 + logN2;
+    using Tl = Tile<LOGL>;
+    constexpr int CW = Tl::CW, E = Tl::E, EPT = Tl::EPT;
+    __shared__ float2 xs[E];
+    const int logN = logN1 + LOGL;
     const int64_t N1 = int64_t(1) << logN1;
-    const int N2 = 1 << logN2;
     const int64_t c0 = int64_t(blockIdx.x) * CW;
     const int64_t n1 = blockIdx.y;
     const int64_t p = blockIdx.z;
     const IO* ua = u + 2 * p * T * D;
     const bool has_b = 2 * p + 1 < B;
-    // rows n2 with n1 + N1 n2 < T hold inputs; the rest is zero padding
+    const IO* ub = has_b ? ua + T * D : ua;
+    // rows n2 with n1 + N1 n2 < T hold inputs; the rest is zero padding.
+    // Branch-free loads (padding reads element 0 and is discarded), so that
+    // all of them are in flight together.
     const int rows = static_cast<int>((T - n1 + N1 - 1) / N1);
-    for (int q = threadIdx.x; q < N2 * CW; q += kThreads) {
+    float2 v[EPT];
+#pragma unroll
+    for (int i = 0; i < EPT; ++i) {
+        const int q = threadIdx.x + i * kThreads;
         const int ch = q % CW, n2 = q / CW;
         const int64_t c = c0 + ch;
-        float2 v = make_float2(0.f, 0.f);
-        if (n2 < rows && c < D) {
-            const int64_t off = (n1 + N1 * n2) * D + c;
-            v.x = io_load(ua + off);
-            if (has_b) v.y = io_load(ua + T * D + off);
-        }
-        xs[brev(n2, logN2) * CW + ch] = v;
+        const bool ok = (E % kThreads == 0 || q < E) && n2 < rows && c < D;
+        const int64_t off = ok ? (n1 + N1 * n2) * D + c : 0;
+        const float a = io_load(ua + off), b = io_load(ub + off);
+        v[i] = make_float2(ok ? a : 0.f, ok && has_b ? b : 0.f);
+    }
+    float2 wv[EPT];  // omega_N^(n1 f2) of the outputs, loaded with the inputs
+#pragma unroll
+    for (int i = 0; i < EPT; ++i) {
+        const int q = threadIdx.x + i * kThreads;
+        wv[i] = twiddle<false>(tw, E % kThreads == 0 || q < E ? n1 * (q / CW) : 0);
+    }
+#pragma unroll
+    for (int i = 0; i < EPT; ++i) {
+        const int q = threadIdx.x + i * kThreads;
+        if (E % kThreads == 0 || q < E) xs[q] = v[i];
     }
     __syncthreads();
-    fft_dit<CW, false>(xs, logN2, tw, logN);
+    fft_tile<LOGL, false>(xs, tw, logN);
     float2* zp = Z + (p << logN) * D;
-    for (int q = threadIdx.x; q < N2 * CW; q += kThreads) {
+#pragma unroll
+    for (int i = 0; i < EPT; ++i) {
+        const int q = threadIdx.x + i * kThreads;
         const int ch = q % CW, f2 = q / CW;
         const int64_t c = c0 + ch;
-        if (c < D)
-            zp[((int64_t(f2) << logN1) + n1) * D + c] =
-                cmul(xs[f2 * CW + ch], twiddle<false>(tw, n1 * f2));
+        if ((E % kThreads == 0 || q < E) && c < D)
+            zp[((int64_t(f2) << logN1) + n1) * D + c] = cmul(xs[q], wv[i]);
     }
 }
 
 // ------------------------------------------------------------ pass B
-// Row transforms: workgroup = (CW channels, row f2, pair p).  CONV = false:
-// forward only, the result is the filter spectrum (in place).  CONV = true:
-// forward, times the filter spectrum, inverse, times omega_N^(-n1 f2).
-template <int CW, bool CONV>
+// Row transforms: workgroup = (CW channels, row f2, pair p); N1 = 2^LOGL.
+// CONV = false: forward only, the result is the filter spectrum (in place).
+// CONV = true: forward, times the filter spectrum (loaded up front), inverse,
+// times omega_N^(-n1 f2).
+template <int LOGL, bool CONV>
 __global__ __launch_bounds__(kThreads) void fft_rows_kernel(float2* __restrict__ Z,
                                                             const float2* __restrict__ H,
-                                                            int64_t D, int logN1, int logN2,
+                                                            int64_t D, int logN2,
                                                             const float2* __restrict__ tw)
 {
-    extern __shared__ float2 xs[];  // [N1][CW]
-    const int logN = logN1 + logN2;
-    const int N1 = 1 << logN1;
+    using Tl = Tile<LOGL>;
+    constexpr int CW = Tl::CW, E = Tl::E, EPT = Tl::EPT;
+    __shared__ float2 xs[E];
+    const int logN = LOGL + logN2;
     const int64_t c0 = int64_t(blockIdx.x) * CW;
     const int64_t f2 = blockIdx.y;
     const int64_t p = blockIdx.z;
-    float2* zr = Z + ((p << logN) + (f2 << logN1)) * D;
-    for (int q = threadIdx.x; q < N1 * CW; q += kThreads) {
-        const int ch = q % CW, n1 = q / CW;
+    float2* zr = Z + ((p << logN) + (f2 << LOGL)) * D;
+    const float2* hr = H + (f2 << LOGL) * D;
+    float2 v[EPT], hv[EPT];
+#pragma unroll
+    for (int i = 0; i < EPT; ++i) {
+        const int q = threadIdx.x + i * kThreads;
+        const int ch = q % CW, n = q / CW;
         const int64_t c = c0 + ch;
-        xs[brev(n1, logN1) * CW + ch] = c < D ? zr[int64_t(n1) * D + c] : make_float2(0.f, 0.f);
+        const bool ok = (E % kThreads == 0 || q < E) && c < D;
+        v[i] = ok ? zr[int64_t(n) * D + c] : make_float2(0.f, 0.f);
+        if (CONV) hv[i] = ok ? hr[int64_t(n) * D + c] : make_float2(0.f, 0.f);
+    }
+    float2 wv[EPT];  // omega_N^(-n1 f2) of the outputs, loaded with the inputs
+    if (CONV) {
+#pragma unroll
+        for (int i = 0; i < EPT; ++i) {
+            const int q = threadIdx.x + i * kThreads;
+            wv[i] = twiddle<true>(tw, E % kThreads == 0 || q < E ? f2 * (q / CW) : 0);
+        }
+    }
+#pragma unroll
+    for (int i = 0; i < EPT; ++i) {
+        const int q = threadIdx.x + i * kThreads;
+        if (E % kThreads == 0 || q < E) xs[q] = v[i];
     }
     __syncthreads();
-    fft_dit<CW, false>(xs, logN1, tw, logN);
+    fft_tile<LOGL, false>(xs, tw, logN);
     if (!CONV) {
-        for (int q = threadIdx.x; q < N1 * CW; q += kThreads) {
+#pragma unroll
+        for (int i = 0; i < EPT; ++i) {
+            const int q = threadIdx.x + i * kThreads;
             const int ch = q % CW, f1 = q / CW;
             const int64_t c = c0 + ch;
-            if (c < D) zr[int64_t(f1) * D + c] = xs[f1 * CW + ch];
+            if ((E % kThreads == 0 || q < E) && c < D) zr[int64_t(f1) * D + c] = xs[q];
         }
         return;
     }
-    const float2* hr = H + (f2 << logN1) * D;
-    for (int q = threadIdx.x; q < N1 * CW; q += kThreads) {
-        const int ch = q % CW, f1 = q / CW;
-        const int64_t c = c0 + ch;
-        if (c < D) xs[f1 * CW + ch] = cmul(xs[f1 * CW + ch], hr[int64_t(f1) * D + c]);
+#pragma unroll
+    for (int i = 0; i < EPT; ++i) {
+        const int q = threadIdx.x + i * kThreads;
+        if (E % kThreads == 0 || q < E) xs[q] = cmul(xs[q], hv[i]);
     }
     __syncthreads();
-    fft_dif<CW, true>(xs, logN1, tw, logN);
-    for (int q = threadIdx.x; q < N1 * CW; q += kThreads) {
+    fft_tile<LOGL, true>(xs, tw, logN);
+#pragma unroll
+    for (int i = 0; i < EPT; ++i) {
+        const int q = threadIdx.x + i * kThreads;
         const int ch = q % CW, n1 = q / CW;
         const int64_t c = c0 + ch;
-        if (c < D)
-            zr[int64_t(n1) * D + c] =
-                cmul(xs[brev(n1, logN1) * CW + ch], twiddle<true>(tw, f2 * n1));
+        if ((E % kThreads == 0 || q < E) && c < D)
+            zr[int64_t(n1) * D + c] = cmul(xs[q], wv[i]);
     }
 }
 
 // ------------------------------------------------------------ pass C
 // Inverse column transforms: workgroup = (CW channels, column n1, pair p);
 // the real part is row 2p's output, the imaginary part row 2p+1's.
-template <typename IO, int CW>
+template <typename IO, int LOGL>
 __global__ __launch_bounds__(kThreads) void fft_cols_inv_kernel(const float2* __restrict__ Z,
                                                                 int64_t B, int64_t T, int64_t D,
-                                                                int logN1, int logN2,
+                                                                int logN1,
                                                                 const float2* __restrict__ tw,
                                                                 IO* __restrict__ y)
 {
-    extern __shared__ float2 xs[];  // [N2][CW]
-    const int logN = logN1 + logN2;
+    using Tl = Tile<LOGL>;
+    constexpr int CW = Tl::CW, E = Tl::E, EPT = Tl::EPT;
+    __shared__ float2 xs[E];
+    const int logN = logN1 + LOGL;
     const int64_t N1 = int64_t(1) << logN1;
-    const int N2 = 1 << logN2;
     const int64_t c0 = int64_t(blockIdx.x) * CW;
     const int64_t n1 = blockIdx.y;
     const int64_t p = blockIdx.z;
     const float2* zp = Z + (p << logN) * D;
-    for (int q = threadIdx.x; q < N2 * CW; q += kThreads) {
+    float2 v[EPT];
+#pragma unroll
+    for (int i = 0; i < EPT; ++i) {
+        const int q = threadIdx.x + i * kThreads;
         const int ch = q % CW, f2 = q / CW;
         const int64_t c = c0 + ch;
-        xs[brev(f2, logN2) * CW + ch] =
-            c < D ? zp[((int64_t(f2) << logN1) + n1) * D + c] : make_float2(0.f, 0.f);
+        v[i] = (E % kThreads == 0 || q < E) && c < D ? zp[((int64_t(f2) << logN1) + n1) * D + c]
+                                                     : make_float2(0.f, 0.f);
+    }
+#pragma unroll
+    for (int i = 0; i < EPT; ++i) {
+        const int q = threadIdx.x + i * kThreads;
+        if (E % kThreads == 0 || q < E) xs[q] = v[i];
     }
     __syncthreads();
-    fft_dit<CW, true>(xs, logN2, tw, logN);
+    fft_tile<LOGL, true>(xs, tw, logN);
     const float scale = 1.f / static_cast<float>(int64_t(1) << logN);  // exact power of two
     const int rows = static_cast<int>((T - n1 + N1 - 1) / N1);
     IO* ya = y + 2 * p * T * D;
     const bool has_b = 2 * p + 1 < B;
-    for (int q = threadIdx.x; q < rows * CW; q += kThreads) {
+#pragma unroll
+    for (int i = 0; i < EPT; ++i) {
+        const int q = threadIdx.x + i * kThreads;
         const int ch = q % CW, n2 = q / CW;
         const int64_t c = c0 + ch;
-        if (c < D) {
-            const float2 v = xs[n2 * CW + ch];
+        if ((E % kThreads == 0 || q < E) && n2 < rows && c < D) {
+            const float2 r = xs[q];
             const int64_t off = (n1 + N1 * n2) * D + c;
-            io_store(ya + off, v.x * scale);
-            if (has_b) io_store(ya + T * D + off, v.y * scale);
+            io_store(ya + off, r.x * scale);
+            if (has_b) io_store(ya + T * D + off, r.y * scale);
         }
     }
 }
@@ -411,6 +483,18 @@ __global__ __launch_bounds__(kThreads) void fft_state_kernel(const IO* __restric
     for (int r = 0; r < kSR; ++r)
 #pragma unroll
         for (int i = 0; i < kSM; ++i) acc[r][i] = make_float2(0.f, 0.f);
+    // one step k: acc += lambda^(T-1-k) u[., k], then the power advances
+    auto step = [&](float2 (&pw)[kSM], const float (&uv)[kSR]) {
+#pragma unroll
+        for (int i = 0; i < kSM; ++i) {
+#pragma unroll
+            for (int r = 0; r < kSR; ++r) {
+                acc[r][i].x = fmaf(pw[i].x, uv[r], acc[r][i].x);
+                acc[r][i].y = fmaf(pw[i].y, uv[r], acc[r][i].y);
+            }
+            pw[i] = cmul(pw[i], l[i]);
+        }
+    };
     const int64_t k_lo = part * part_len;
     const int64_t k_hi = k_lo + part_len < T ? k_lo + part_len : T;
     for (int64_t hi = k_hi; hi > k_lo; hi -= kSSeg) {
@@ -419,19 +503,42 @@ __global__ __launch_bounds__(kThreads) void fft_state_kernel(const IO* __restric
 #pragma unroll
         for (int i = 0; i < kSM; ++i)
             pw[i] = n0 + i < d ? polar_pow(pol[cc * d + n0 + i], T - hi) : make_float2(0.f, 0.f);
-#pragma unroll 4
-        for (int64_t k = hi - 1; k >= lo; --k) {
+        // the top (hi - lo) mod 8 steps one by one, then blocks of 8 steps
+        // with the next block's inputs loaded while the current one is used
+        const int64_t nblk = (hi - lo) / kPf;
+        int64_t k = hi - 1;
+        for (; k >= lo + nblk * kPf; --k) {
             float uv[kSR];
 #pragma unroll
             for (int r = 0; r < kSR; ++r) uv[r] = io_load(ur[r] + k * D);
+            step(pw, uv);
+        }
+        if (nblk > 0) {
+            // two buffers in turn: block i + 1 loads while block i is used
+            float ba[kPf][kSR], bb[kPf][kSR];
+            auto load = [&](float (&buf)[kPf][kSR], int64_t kk) {
 #pragma unroll
-            for (int i = 0; i < kSM; ++i) {
+                for (int s = 0; s < kPf; ++s)
 #pragma unroll
-                for (int r = 0; r < kSR; ++r) {
-                    acc[r][i].x = fmaf(pw[i].x, uv[r], acc[r][i].x);
-                    acc[r][i].y = fmaf(pw[i].y, uv[r], acc[r][i].y);
-                }
-                pw[i] = cmul(pw[i], l[i]);
+                    for (int r = 0; r < kSR; ++r) buf[s][r] = io_load(ur[r] + (kk - s) * D);
+                // keep the loads here, ahead of the arithmetic that follows
+                asm volatile("" ::: "memory");
+                __builtin_amdgcn_sched_barrier(0);
+            };
+            auto use = [&](const float (&buf)[kPf][kSR]) {
+#pragma unroll
+                for (int s = 0; s < kPf; ++s) step(pw, buf[s]);
+            };
+            load(ba, k);
+            for (int64_t blk = 0; blk < nblk; blk += 2) {
+                const bool more1 = blk + 1 < nblk, more2 = blk + 2 < nblk;
+                load(bb, more1 ? k - kPf : k);  // past the last block: reload (unused)
+                use(ba);
+                k -= kPf;
+                if (!more1) break;
+                load(ba, more2 ? k - kPf : k);
+                use(bb);
+                k -= kPf;
             }
         }
     }
@@ -464,9 +571,6 @@ __global__ __launch_bounds__(kThreads) void fft_zero_kernel(float2* __restrict__
     if (i < n) p[i] = make_float2(0.f, 0.f);
 }
 
-// channels per workgroup of a transform of length 2^logL (64 KiB of LDS)
-int cw_for(int logL) { return (1 << logL) * 32 <= kLdsElems ? 32 : (1 << logL) * 16 <= kLdsElems ? 16 : 8; }
-
 bool blocks_for(int64_t n, int64_t per, uint32_t* g)
 {
     const int64_t b = (n + per - 1) / per;
@@ -477,66 +581,69 @@ bool blocks_for(int64_t n, int64_t per, uint32_t* g)
 
 size_t align256(size_t x) { return (x + 255) / 256 * 256; }
 
-template <typename IO, int CW>
+#define LH_FFT_LENGTHS(X) X(0) X(1) X(2) X(3) X(4) X(5) X(6) X(7) X(8) X(9) X(10)
+
+template <typename IO>
 hipError_t cols_fwd(const IO* u, int64_t B, int64_t T, int64_t D, int logN1, int logN2,
                     const float2* tw, float2* Z, int64_t npair, hipStream_t stream)
 {
     uint32_t gx;
-    if (!blocks_for(D, CW, &gx)) return hipErrorInvalidConfiguration;
-    const dim3 grid(gx, 1u << logN1, static_cast<uint32_t>(npair));
-    const size_t shm = sizeof(float2) * (size_t(1) << logN2) * CW;
-    hipLaunchKernelGGL((fft_cols_fwd_kernel<IO, CW>), grid, dim3(kThreads), shm, stream, u, B, T, D,
-                       logN1, logN2, tw, Z);
-    return hipGetLastError();
-}
-
-template <typename IO>
-hipError_t cols_fwd_any(const IO* u, int64_t B, int64_t T, int64_t D, int logN1, int logN2,
-                        const float2* tw, float2* Z, int64_t npair, hipStream_t stream)
-{
-    switch (cw_for(logN2)) {
-        case 32: return cols_fwd<IO, 32>(u, B, T, D, logN1, logN2, tw, Z, npair, stream);
-        case 16: return cols_fwd<IO, 16>(u, B, T, D, logN1, logN2, tw, Z, npair, stream);
-        default: return cols_fwd<IO, 8>(u, B, T, D, logN1, logN2, tw, Z, npair, stream);
+    switch (logN2) {
+#define LH_CASE(K)                                                                               \
+    case K:                                                                                      \
+        if (!blocks_for(D, Tile<K>::CW, &gx)) return hipErrorInvalidConfiguration;              \
+        hipLaunchKernelGGL((fft_cols_fwd_kernel<IO, K>),                                         \
+                           dim3(gx, 1u << logN1, static_cast<uint32_t>(npair)), dim3(kThreads),  \
+                           0, stream, u, B, T, D, logN1, tw, Z);                                 \
+        break;
+        LH_FFT_LENGTHS(LH_CASE)
+#undef LH_CASE
+        default: return hipErrorInvalidValue;
     }
-}
-
-template <int CW, bool CONV>
-hipError_t rows(float2* Z, const float2* H, int64_t D, int logN1, int logN2, const float2* tw,
-                int64_t npair, hipStream_t stream)
-{
-    uint32_t gx;
-    if (!blocks_for(D, CW, &gx)) return hipErrorInvalidConfiguration;
-    const dim3 grid(gx, 1u << logN2, static_cast<uint32_t>(npair));
-    const size_t shm = sizeof(float2) * (size_t(1) << logN1) * CW;
-    hipLaunchKernelGGL((fft_rows_kernel<CW, CONV>), grid, dim3(kThreads), shm, stream, Z, H, D,
-                       logN1, logN2, tw);
     return hipGetLastError();
 }
 
 template <bool CONV>
-hipError_t rows_any(float2* Z, const float2* H, int64_t D, int logN1, int logN2,
-                    const float2* tw, int64_t npair, hipStream_t stream)
+hipError_t rows(float2* Z, const float2* H, int64_t D, int logN1, int logN2, const float2* tw,
+                int64_t npair, hipStream_t stream)
 {
-    switch (cw_for(logN1)) {
-        case 32: return rows<32, CONV>(Z, H, D, logN1, logN2, tw, npair, stream);
-        case 16: return rows<16, CONV>(Z, H, D, logN1, logN2, tw, npair, stream);
-        default: return rows<8, CONV>(Z, H, D, logN1, logN2, tw, npair, stream);
+    uint32_t gx;
+    switch (logN1) {
+#define LH_CASE(K)                                                                               \
+    case K:                                                                                      \
+        if (!blocks_for(D, Tile<K>::CW, &gx)) return hipErrorInvalidConfiguration;              \
+        hipLaunchKernelGGL((fft_rows_kernel<K, CONV>),                                           \
+                           dim3(gx, 1u << logN2, static_cast<uint32_t>(npair)), dim3(kThreads),  \
+                           0, stream, Z, H, D, logN2, tw);                                       \
+        break;
+        LH_FFT_LENGTHS(LH_CASE)
+#undef LH_CASE
+        default: return hipErrorInvalidValue;
     }
+    return hipGetLastError();
 }
 
-template <typename IO, int CW>
+template <typename IO>
 hipError_t cols_inv(const float2* Z, int64_t B, int64_t T, int64_t D, int logN1, int logN2,
                     const float2* tw, IO* y, int64_t npair, hipStream_t stream)
 {
     uint32_t gx;
-    if (!blocks_for(D, CW, &gx)) return hipErrorInvalidConfiguration;
-    const dim3 grid(gx, 1u << logN1, static_cast<uint32_t>(npair));
-    const size_t shm = sizeof(float2) * (size_t(1) << logN2) * CW;
-    hipLaunchKernelGGL((fft_cols_inv_kernel<IO, CW>), grid, dim3(kThreads), shm, stream, Z, B, T, D,
-                       logN1, logN2, tw, y);
+    switch (logN2) {
+#define LH_CASE(K)                                                                               \
+    case K:                                                                                      \
+        if (!blocks_for(D, Tile<K>::CW, &gx)) return hipErrorInvalidConfiguration;              \
+        hipLaunchKernelGGL((fft_cols_inv_kernel<IO, K>),                                         \
+                           dim3(gx, 1u << logN1, static_cast<uint32_t>(npair)), dim3(kThreads),  \
+                           0, stream, Z, B, T, D, logN1, tw, y);                                 \
+        break;
+        LH_FFT_LENGTHS(LH_CASE)
+#undef LH_CASE
+        default: return hipErrorInvalidValue;
+    }
     return hipGetLastError();
 }
+
+#undef LH_FFT_LENGTHS
 
 template <typename IO>
 hipError_t run(const float2* lam, const float2* R, const float* h0, const IO* u, int64_t B,
@@ -565,22 +672,16 @@ hipError_t run(const float2* lam, const float2* R, const float* h0, const IO* u,
     hipLaunchKernelGGL(fft_filter_kernel, dim3(gc, gt), dim3(kThreads), 0, stream, lam, R, h0, pol,
                        D, static_cast<int>(d), T, hh);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    if ((e = cols_fwd_any<float>(hh, 1, T, D, p.logN1, p.logN2, tw, H, 1, stream)) != hipSuccess)
+    if ((e = cols_fwd<float>(hh, 1, T, D, p.logN1, p.logN2, tw, H, 1, stream)) != hipSuccess)
         return e;
-    if ((e = rows_any<false>(H, nullptr, D, p.logN1, p.logN2, tw, 1, stream)) != hipSuccess)
-        return e;
+    if ((e = rows<false>(H, H, D, p.logN1, p.logN2, tw, 1, stream)) != hipSuccess) return e;
 
     // outputs
-    if ((e = cols_fwd_any<IO>(u, B, T, D, p.logN1, p.logN2, tw, Z, p.npair, stream)) != hipSuccess)
+    if ((e = cols_fwd<IO>(u, B, T, D, p.logN1, p.logN2, tw, Z, p.npair, stream)) != hipSuccess)
         return e;
-    if ((e = rows_any<true>(Z, H, D, p.logN1, p.logN2, tw, p.npair, stream)) != hipSuccess)
+    if ((e = rows<true>(Z, H, D, p.logN1, p.logN2, tw, p.npair, stream)) != hipSuccess) return e;
+    if ((e = cols_inv<IO>(Z, B, T, D, p.logN1, p.logN2, tw, y, p.npair, stream)) != hipSuccess)
         return e;
-    switch (cw_for(p.logN2)) {
-        case 32: e = cols_inv<IO, 32>(Z, B, T, D, p.logN1, p.logN2, tw, y, p.npair, stream); break;
-        case 16: e = cols_inv<IO, 16>(Z, B, T, D, p.logN1, p.logN2, tw, y, p.npair, stream); break;
-        default: e = cols_inv<IO, 8>(Z, B, T, D, p.logN1, p.logN2, tw, y, p.npair, stream); break;
-    }
-    if (e != hipSuccess) return e;
 
     // state
     const int nmc = static_cast<int>((d + kSM - 1) / kSM);
