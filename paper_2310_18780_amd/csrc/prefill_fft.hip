@@ -330,20 +330,27 @@ __global__ __launch_bounds__(kThreads) void fft_cols_fwd_kernel(const IO* __rest
 // Row transforms: workgroup = (CW channels, row f2, pair p); N1 = 2^LOGL.
 // CONV = false: forward only, the result is the filter spectrum (in place).
 // CONV = true: forward, times the filter spectrum (loaded up front), inverse,
-// times omega_N^(-n1 f2).
+// times omega_N^(-n1 f2).  One-dimensional grid: workgroup i runs on XCD
+// i mod 8, and the npair workgroups of a (channel group, row) tile are 8
+// apart, so they run together on one XCD and read the tile's filter spectrum
+// from HBM once (the rest from that XCD's L2).
 template <int LOGL, bool CONV>
 __global__ __launch_bounds__(kThreads) void fft_rows_kernel(float2* __restrict__ Z,
                                                             const float2* __restrict__ H,
-                                                            int64_t D, int logN2,
+                                                            int64_t D, int logN2, int64_t npair,
                                                             const float2* __restrict__ tw)
 {
     using Tl = Tile<LOGL>;
     constexpr int CW = Tl::CW, E = Tl::E, EPT = Tl::EPT;
     __shared__ float2 xs[E];
     const int logN = LOGL + logN2;
-    const int64_t c0 = int64_t(blockIdx.x) * CW;
-    const int64_t f2 = blockIdx.y;
-    const int64_t p = blockIdx.z;
+    const int64_t gx = (D + CW - 1) / CW;
+    const int64_t id = blockIdx.x;
+    const int64_t tile = id / (8 * npair) * 8 + id % 8;
+    if (tile >= (gx << logN2)) return;
+    const int64_t p = id / 8 % npair;
+    const int64_t c0 = tile % gx * CW;
+    const int64_t f2 = tile / gx;
     float2* zr = Z + ((p << logN) + (f2 << LOGL)) * D;
     const float2* hr = H + (f2 << LOGL) * D;
     float2 v[EPT], hv[EPT];
@@ -611,10 +618,11 @@ hipError_t rows(float2* Z, const float2* H, int64_t D, int logN1, int logN2, con
     switch (logN1) {
 #define LH_CASE(K)                                                                               \
     case K:                                                                                      \
-        if (!blocks_for(D, Tile<K>::CW, &gx)) return hipErrorInvalidConfiguration;              \
-        hipLaunchKernelGGL((fft_rows_kernel<K, CONV>),                                           \
-                           dim3(gx, 1u << logN2, static_cast<uint32_t>(npair)), dim3(kThreads),  \
-                           0, stream, Z, H, D, logN2, tw);                                       \
+        if (!blocks_for(((D + Tile<K>::CW - 1) / Tile<K>::CW << logN2) * npair, 8 * npair, &gx) \
+            || int64_t(gx) * 8 * npair > 0x7fffffff)                                            \
+            return hipErrorInvalidConfiguration;                                                 \
+        hipLaunchKernelGGL((fft_rows_kernel<K, CONV>), dim3(gx * 8 * uint32_t(npair)),          \
+                           dim3(kThreads), 0, stream, Z, H, D, logN2, npair, tw);                \
         break;
         LH_FFT_LENGTHS(LH_CASE)
 #undef LH_CASE
