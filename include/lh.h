@@ -190,6 +190,79 @@ lh_status lh_step(const lh_c32* lambda, const lh_c32* R, const float* h0,
                   int64_t B, int64_t D, int64_t d, lh_dtype io_dtype,
                   void* stream);
 
+/* Largest modal order the companion form accepts (companion order 2d <= 32). */
+#define LH_COMPANION_MAX_MODES 16
+
+/*
+ * Companion (rational) form of the distilled filters (App. "From Transfer
+ * Function to State-Space", eq. "ssm_canon"; canonization of a modal SSM).
+ * The real filter h_0 = h0, h_t = Re sum_n R_n lambda_n^(t-1) is the impulse
+ * response of a real system of order 2d (each pole with its conjugate,
+ * residues R_n / 2 and conj(R_n) / 2, App. B.1) whose transfer function in
+ * w = z^-1 is
+ *
+ *   H(w) = h0 + (beta_1 w + ... + beta_2d w^2d) / (1 + a_1 w + ... + a_2d w^2d)
+ *
+ * This call writes, per channel, a[c, m-1] = a_m and beta[c, m-1] = beta_m
+ * (m = 1..2d), computed in float64 from the complex64 poles and residues.
+ *
+ *   lambda, R : [D, d] complex64;  a, beta : out [D, 2d] float64
+ *   D >= 1, 1 <= d <= LH_COMPANION_MAX_MODES
+ * Outputs must not overlap each other or the inputs.  One kernel launch; no
+ * workspace; same execution and error rules as lh_step.
+ *
+ * Numerical range: p's coefficients grow like binomial coefficients and the
+ * companion state like the impulse response of 1/p, far beyond the outputs it
+ * combines, so even in float64 the form meets a 1e-4 relative accuracy only
+ * for small orders (measured over 1500 steps with pole angles spread over
+ * [0, pi]: d <= 8 at pole radii up to 0.9999; d = 16 loses it near the unit
+ * circle).  The modal calls above do not have this limit.
+ */
+lh_status lh_companion_coeffs(const lh_c32* lambda, const lh_c32* R, int64_t D, int64_t d,
+                              double* a, double* beta, void* stream);
+
+/*
+ * Companion decode step (Lemma "efficient_recurrence"), per (b, c):
+ *   y_t[b,c]      = sum_m beta[c,m] state[b,c,m] + h0[c] u_t[b,c]
+ *   state[b,c,:]  = (u_t[b,c] - sum_m a[c,m] state[b,c,m], state[b,c,0], ...,
+ *                    state[b,c,2d-2])                               (in place)
+ * in float64, y_t rounded to io_dtype.
+ *
+ *   a, beta : [D, 2d] float64 (lh_companion_coeffs);  h0 : [D] float32
+ *   state   : in/out [B, D, 2d] float64, 16-byte aligned
+ *   u_t, y_t: [B, D] (io_dtype)
+ * y_t must not overlap any other buffer; state must not overlap a, beta, h0
+ * or u_t.  One kernel launch; no workspace; same execution and error rules
+ * as lh_step.
+ */
+lh_status lh_companion_step(const double* a, const double* beta, const float* h0,
+                            double* state, const void* u_t, void* y_t,
+                            int64_t B, int64_t D, int64_t d, lh_dtype io_dtype, void* stream);
+
+/* Workspace bytes of lh_companion_init: T D 8 (the taps of 1/p); 0 when
+ * T == 0, (size_t)-1 for invalid sizes. */
+size_t lh_companion_init_workspace_bytes(int64_t D, int64_t d, int64_t T);
+
+/*
+ * Companion state after a prompt without stepping (Proposition "fast_init"):
+ *   state[b,c,j] = v_{T-1-j},  v = g * u[b,:,c],  j = 0..2d-1
+ * with g the impulse response of 1/p (g_0 = 1, g_t = -sum_m a_m g_{t-m}) and
+ * v_t = 0 for t < 0; the state lh_companion_step reaches from zero after the
+ * T prompt inputs.  Prompt outputs come from lh_prefill or lh_prefill_fft
+ * (the same filter).
+ *
+ *   a        : [D, 2d] float64;  u : [B, T, D] (io_dtype)
+ *   state    : out [B, D, 2d] float64, 16-byte aligned
+ *   workspace: lh_companion_init_workspace_bytes(D, d, T) bytes, 256-byte
+ *              aligned (NULL allowed when that is 0)
+ *   T >= 0; T == 0 zeroes the state
+ * state and workspace must not overlap each other or the inputs.  Two kernel
+ * launches; same execution and error rules as lh_prefill.
+ */
+lh_status lh_companion_init(const double* a, const void* u, int64_t B, int64_t D, int64_t d,
+                            int64_t T, lh_dtype io_dtype, double* state, void* workspace,
+                            size_t workspace_bytes, void* stream);
+
 /*
  * Multi-head decode step (Sec. 5, "Multi-head Long Convolutions": the
  * projections q, k, v of width D = M N are split into M heads of N channels;

@@ -32,6 +32,10 @@ __all__ = [
     "step",
     "mh_step",
     "distill",
+    "companion_coeffs",
+    "companion_step",
+    "companion_init_workspace_bytes",
+    "companion_init",
     "STATUS",
 ]
 
@@ -97,6 +101,14 @@ def lib() -> ctypes.CDLL:
     L.lh_mh_step.restype = ctypes.c_int
     L.lh_distill.argtypes = [vp, vp, vp, vp, i64, i64, i64, vp, vp, vp, vp, vp, vp]
     L.lh_distill.restype = ctypes.c_int
+    L.lh_companion_coeffs.argtypes = [vp, vp, i64, i64, vp, vp, vp]
+    L.lh_companion_coeffs.restype = ctypes.c_int
+    L.lh_companion_step.argtypes = [vp, vp, vp, vp, vp, vp, i64, i64, i64, ctypes.c_int, vp]
+    L.lh_companion_step.restype = ctypes.c_int
+    L.lh_companion_init_workspace_bytes.argtypes = [i64, i64, i64]
+    L.lh_companion_init_workspace_bytes.restype = sz
+    L.lh_companion_init.argtypes = [vp, vp, i64, i64, i64, i64, ctypes.c_int, vp, vp, sz, vp]
+    L.lh_companion_init.restype = ctypes.c_int
     _lib = L
     return L
 
@@ -268,3 +280,64 @@ def distill(A, theta, R, target, loss, dA, dtheta, dR, hhat=None, stream=None) -
                             L, loss.data_ptr(), dA.data_ptr(), dtheta.data_ptr(), dR.data_ptr(),
                             hhat.data_ptr() if hhat is not None else None,
                             _stream(A.device, stream)))
+
+
+def companion_coeffs(lam, R, a, beta, stream=None) -> None:
+    """Rational coefficients of the filters' companion form
+    (``lh_companion_coeffs``): ``a, beta [D, 2d]`` float64 from ``lam, R [D, d]``."""
+    import torch
+
+    D, d = lam.shape
+    _need(lam, "lam", torch.complex64, (D, d))
+    _need(R, "R", torch.complex64, (D, d))
+    _need(a, "a", torch.float64, (D, 2 * d))
+    _need(beta, "beta", torch.float64, (D, 2 * d))
+    _check(lib().lh_companion_coeffs(lam.data_ptr(), R.data_ptr(), D, d, a.data_ptr(),
+                                     beta.data_ptr(), _stream(lam.device, stream)))
+
+
+def companion_step(a, beta, h0, state, u_t, y_t, stream=None) -> None:
+    """One companion decode step (``lh_companion_step``); ``state [B, D, 2d]``
+    float64 in place."""
+    import torch
+
+    B, D, order = state.shape
+    _need(a, "a", torch.float64, (D, order))
+    _need(beta, "beta", torch.float64, (D, order))
+    _need(h0, "h0", torch.float32, (D,))
+    _need(state, "state", torch.float64, (B, D, order))
+    _need(u_t, "u_t", u_t.dtype, (B, D))
+    _need(y_t, "y_t", u_t.dtype, (B, D))
+    if order % 2:
+        raise ValueError(f"companion order must be even (2d), got {order}")
+    _check(lib().lh_companion_step(a.data_ptr(), beta.data_ptr(), h0.data_ptr(), state.data_ptr(),
+                                   u_t.data_ptr(), y_t.data_ptr(), B, D, order // 2,
+                                   _io_dtype(u_t), _stream(u_t.device, stream)))
+
+
+def companion_init_workspace_bytes(D: int, d: int, T: int) -> int:
+    n = lib().lh_companion_init_workspace_bytes(D, d, T)
+    if n == ctypes.c_size_t(-1).value:
+        raise LHError(1, f"invalid sizes for the companion initialisation D={D} d={d} T={T}")
+    return int(n)
+
+
+def companion_init(a, u, state, workspace=None, stream=None) -> None:
+    """Companion state after the prompt ``u [B, T, D]`` (``lh_companion_init``,
+    Proposition "fast_init")."""
+    import torch
+
+    B, T, D = u.shape
+    order = a.shape[1]
+    _need(a, "a", torch.float64, (D, order))
+    _need(u, "u", u.dtype, (B, T, D))
+    _need(state, "state", torch.float64, (B, D, order))
+    if order % 2:
+        raise ValueError(f"companion order must be even (2d), got {order}")
+    need = companion_init_workspace_bytes(D, order // 2, T)
+    if need > 0 and workspace is None:
+        workspace = torch.empty(need, dtype=torch.uint8, device=u.device)
+    ws_ptr = workspace.data_ptr() if workspace is not None else None
+    ws_len = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    _check(lib().lh_companion_init(a.data_ptr(), u.data_ptr(), B, D, order // 2, T, _io_dtype(u),
+                                   state.data_ptr(), ws_ptr, ws_len, _stream(u.device, stream)))

@@ -14,7 +14,8 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "liblh.so")
 
-SOURCES = ["lh_api.cpp", "decode.hip", "prefill.hip", "prefill_mfma.hip", "prefill_fft.hip", "multihead.hip", "distill.hip"]
+SOURCES = ["lh_api.cpp", "decode.hip", "prefill.hip", "prefill_mfma.hip", "prefill_fft.hip", "multihead.hip", "distill.hip",
+           "companion.hip"]
 
 # -packed-fp32-ops: no v_pk_{add,mul,fma}_f32 in the generated code (the host
 # pass warns that it does not know the feature; that is harmless).

@@ -1,0 +1,284 @@
+// Companion (rational) form of a distilled filter (App. "From Transfer
+// Function to State-Space", eq. "ssm_canon"; Lemma "efficient_recurrence";
+// Proposition "fast_init").
+//
+// The real filter h_0 = h0, h_t = Re sum_n R_n lambda_n^(t-1) is the impulse
+// response of a real system of order 2d: each pole comes with its conjugate
+// and the residues are R_n / 2 and conj(R_n) / 2 (App. B.1).  In w = z^-1 its
+// transfer function is h0 + beta(w) / p(w) with
+//
+//   p(w)    = prod_n q_n(w),   q_n(w) = 1 - 2 Re(lambda_n) w + |lambda_n|^2 w^2
+//   beta(w) = sum_n w (Re R_n - Re(R_n conj(lambda_n)) w) prod_{m != n} q_m(w)
+//
+// (a conjugate pair of partial fractions brought over its real quadratic
+// denominator, then over p), a_m and beta_m the coefficients of w^m, m =
+// 1..2d.  The companion recurrence steps a real state of 2d entries:
+//
+//   y_t = beta . x_t + h0 u_t,   x_{t+1} = (u_t - a . x_t, x_t[0], ..., x_t[2d-2])
+//
+// and the fast initialisation gives the state after a prompt directly:
+// x_T[j] = v_{T-1-j}, v = g * u, g the impulse response of 1 / p.
+//
+// Everything runs in float64.  The coefficients of p grow like binomial
+// coefficients and the impulse response of 1 / p grows polynomially before
+// its poles damp it, so the state becomes far larger than the outputs it
+// combines: float32 loses the 1e-4 accuracy of the modal path from d = 4-8,
+// float64 from d = 16 with poles near the unit circle (the paper flags the
+// form as fragile there).  The modal path is the default; this form serves
+// small orders.
+#include "companion.hpp"
+
+namespace lh {
+namespace {
+
+constexpr int kMaxOrd = 2 * kCompanionMaxModes;
+constexpr int kThreads = 256;
+
+// One 64-thread workgroup per channel; thread k owns the coefficient of w^k.
+__global__ __launch_bounds__(64) void companion_coeffs_kernel(const float2* __restrict__ lam,
+                                                             const float2* __restrict__ R,
+                                                             int d, double* __restrict__ a,
+                                                             double* __restrict__ beta)
+{
+    __shared__ double p[kMaxOrd + 1], q[kMaxOrd + 1], num[kMaxOrd + 1];
+    const int64_t c = blockIdx.x;
+    const int k = threadIdx.x;
+    const int ord = 2 * d;
+    const bool own = k <= ord;
+    const float2* lc = lam + c * d;
+    const float2* rc = R + c * d;
+    // multiply the polynomial in buf by q_n (all threads take part in the barriers)
+    auto times_q = [&](double* buf, int n) {
+        const double lr = lc[n].x, li = lc[n].y;
+        const double c1 = -2.0 * lr, c2 = lr * lr + li * li;
+        double v = 0.0;
+        if (own) {
+            v = buf[k];
+            if (k >= 1) v = fma(c1, buf[k - 1], v);
+            if (k >= 2) v = fma(c2, buf[k - 2], v);
+        }
+        __syncthreads();
+        if (own) buf[k] = v;
+        __syncthreads();
+    };
+    if (own) {
+        p[k] = k == 0 ? 1.0 : 0.0;
+        num[k] = 0.0;
+    }
+    __syncthreads();
+    for (int n = 0; n < d; ++n) times_q(p, n);
+    for (int n = 0; n < d; ++n) {
+        if (own) q[k] = k == 0 ? 1.0 : 0.0;
+        __syncthreads();
+        for (int m = 0; m < d; ++m)
+            if (m != n) times_q(q, m);
+        const double lr = lc[n].x, li = lc[n].y, rr = rc[n].x, ri = rc[n].y;
+        const double e0 = rr, e1 = -(rr * lr + ri * li);  // Re R, -Re(R conj(lambda))
+        if (own) {
+            double v = num[k];
+            if (k >= 1) v = fma(e0, q[k - 1], v);
+            if (k >= 2) v = fma(e1, q[k - 2], v);
+            num[k] = v;
+        }
+        __syncthreads();
+    }
+    if (own && k >= 1) {
+        a[c * ord + k - 1] = p[k];
+        beta[c * ord + k - 1] = num[k];
+    }
+}
+
+// One thread per (b, c) row; the row's 2d state entries in registers.
+template <typename IO, int ORD>
+__global__ __launch_bounds__(kThreads) void companion_step_kernel(
+    const double* __restrict__ a, const double* __restrict__ beta, const float* __restrict__ h0,
+    double* __restrict__ state, const IO* __restrict__ u, IO* __restrict__ y, int64_t B,
+    int64_t D)
+{
+    const int64_t i = int64_t(blockIdx.x) * kThreads + threadIdx.x;
+    if (i >= B * D) return;
+    const int64_t c = i % D;
+    double2* xs = reinterpret_cast<double2*>(state + i * ORD);
+    double x[ORD];
+#pragma unroll
+    for (int m = 0; m < ORD / 2; ++m) {
+        const double2 v = xs[m];
+        x[2 * m] = v.x;
+        x[2 * m + 1] = v.y;
+    }
+    const double* ac = a + c * ORD;
+    const double* bc = beta + c * ORD;
+    const double ut = io_load(u + i);
+    double out = 0.0, fb = 0.0;
+#pragma unroll
+    for (int m = 0; m < ORD; ++m) {
+        out = fma(bc[m], x[m], out);
+        fb = fma(ac[m], x[m], fb);
+    }
+    out = fma(static_cast<double>(h0[c]), ut, out);
+    io_store(y + i, static_cast<float>(out));
+    xs[0] = make_double2(ut - fb, x[0]);
+#pragma unroll
+    for (int m = 1; m < ORD / 2; ++m) xs[m] = make_double2(x[2 * m - 1], x[2 * m]);
+}
+
+// g_t for t < T per channel (one thread per channel): g_0 = 1,
+// g_t = -sum_m a_m g_{t-m}.
+template <int ORD>
+__global__ __launch_bounds__(kThreads) void companion_g_kernel(const double* __restrict__ a,
+                                                              int64_t D, int64_t T,
+                                                              double* __restrict__ g)
+{
+    const int64_t c = int64_t(blockIdx.x) * kThreads + threadIdx.x;
+    if (c >= D) return;
+    double am[ORD], w[ORD];  // w[m] = g_{t-1-m}
+#pragma unroll
+    for (int m = 0; m < ORD; ++m) {
+        am[m] = a[c * ORD + m];
+        w[m] = 0.0;
+    }
+    for (int64_t t = 0; t < T; ++t) {
+        double acc = t == 0 ? 1.0 : 0.0;
+#pragma unroll
+        for (int m = 0; m < ORD; ++m) acc = fma(-am[m], w[m], acc);
+        g[t * D + c] = acc;
+#pragma unroll
+        for (int m = ORD - 1; m > 0; --m) w[m] = w[m - 1];
+        w[0] = acc;
+    }
+}
+
+// state[b, c, j] = v_{T-1-j} = sum_{k <= T-1-j} g_{T-1-j-k} u_k, one thread per
+// (b, c); a window of the 2d taps g_{T-1-j-k} slides along k.
+template <typename IO, int ORD>
+__global__ __launch_bounds__(kThreads) void companion_init_kernel(const double* __restrict__ g,
+                                                                 const IO* __restrict__ u,
+                                                                 int64_t B, int64_t D, int64_t T,
+                                                                 double* __restrict__ state)
+{
+    const int64_t i = int64_t(blockIdx.x) * kThreads + threadIdx.x;
+    if (i >= B * D) return;
+    const int64_t b = i / D, c = i % D;
+    const IO* ub = u + b * T * D + c;
+    double win[ORD], acc[ORD];
+#pragma unroll
+    for (int j = 0; j < ORD; ++j) {
+        win[j] = T - 1 - j >= 0 ? g[(T - 1 - j) * D + c] : 0.0;
+        acc[j] = 0.0;
+    }
+    for (int64_t k = 0; k < T; ++k) {
+        const double uk = io_load(ub + k * D);
+#pragma unroll
+        for (int j = 0; j < ORD; ++j) acc[j] = fma(win[j], uk, acc[j]);
+#pragma unroll
+        for (int j = 0; j < ORD - 1; ++j) win[j] = win[j + 1];
+        const int64_t nx = T - 1 - ORD - k;
+        win[ORD - 1] = nx >= 0 ? g[nx * D + c] : 0.0;
+    }
+    double2* xs = reinterpret_cast<double2*>(state + i * ORD);
+#pragma unroll
+    for (int m = 0; m < ORD / 2; ++m) xs[m] = make_double2(acc[2 * m], acc[2 * m + 1]);
+}
+
+__global__ __launch_bounds__(kThreads) void companion_zero_kernel(double* __restrict__ p,
+                                                                 int64_t n)
+{
+    const int64_t i = int64_t(blockIdx.x) * kThreads + threadIdx.x;
+    if (i < n) p[i] = 0.0;
+}
+
+bool blocks(int64_t n, uint32_t* g)
+{
+    const int64_t b = (n + kThreads - 1) / kThreads;
+    if (b < 1 || b > 0x7fffffff) return false;
+    *g = static_cast<uint32_t>(b);
+    return true;
+}
+
+#define LH_COMPANION_ORDERS(X) \
+    X(2) X(4) X(6) X(8) X(10) X(12) X(14) X(16) X(18) X(20) X(22) X(24) X(26) X(28) X(30) X(32)
+
+template <typename IO>
+hipError_t step_io(const double* a, const double* beta, const float* h0, double* state,
+                   const void* u_t, void* y_t, int64_t B, int64_t D, int64_t d, hipStream_t s)
+{
+    uint32_t g;
+    if (!blocks(B * D, &g)) return hipErrorInvalidConfiguration;
+    switch (2 * d) {
+#define LH_CASE(O)                                                                              \
+    case O:                                                                                     \
+        hipLaunchKernelGGL((companion_step_kernel<IO, O>), dim3(g), dim3(kThreads), 0, s, a,    \
+                           beta, h0, state, static_cast<const IO*>(u_t), static_cast<IO*>(y_t), \
+                           B, D);                                                               \
+        break;
+        LH_COMPANION_ORDERS(LH_CASE)
+#undef LH_CASE
+        default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+template <typename IO>
+hipError_t init_io(const double* a, const void* u, int64_t B, int64_t D, int64_t d, int64_t T,
+                   double* state, double* gbuf, hipStream_t s)
+{
+    uint32_t gc, gr;
+    if (!blocks(D, &gc) || !blocks(B * D, &gr)) return hipErrorInvalidConfiguration;
+    hipError_t e;
+    switch (2 * d) {
+#define LH_CASE(O)                                                                               \
+    case O:                                                                                      \
+        hipLaunchKernelGGL((companion_g_kernel<O>), dim3(gc), dim3(kThreads), 0, s, a, D, T,     \
+                           gbuf);                                                                \
+        if ((e = hipGetLastError()) != hipSuccess) return e;                                     \
+        hipLaunchKernelGGL((companion_init_kernel<IO, O>), dim3(gr), dim3(kThreads), 0, s, gbuf, \
+                           static_cast<const IO*>(u), B, D, T, state);                           \
+        break;
+        LH_COMPANION_ORDERS(LH_CASE)
+#undef LH_CASE
+        default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+#undef LH_COMPANION_ORDERS
+
+}  // namespace
+
+hipError_t launch_companion_coeffs(const float2* lam, const float2* R, int64_t D, int64_t d,
+                                   double* a, double* beta, hipStream_t stream)
+{
+    (void)hipGetLastError();
+    if (D > 0x7fffffff || d < 1 || d > kCompanionMaxModes) return hipErrorInvalidConfiguration;
+    hipLaunchKernelGGL(companion_coeffs_kernel, dim3(static_cast<uint32_t>(D)), dim3(64), 0,
+                       stream, lam, R, static_cast<int>(d), a, beta);
+    return hipGetLastError();
+}
+
+hipError_t launch_companion_step(const double* a, const double* beta, const float* h0,
+                                 double* state, const void* u_t, void* y_t, bool bf16_io,
+                                 int64_t B, int64_t D, int64_t d, hipStream_t stream)
+{
+    (void)hipGetLastError();
+    return bf16_io ? step_io<bf16>(a, beta, h0, state, u_t, y_t, B, D, d, stream)
+                   : step_io<float>(a, beta, h0, state, u_t, y_t, B, D, d, stream);
+}
+
+hipError_t launch_companion_init(const double* a, const void* u, bool bf16_io, int64_t B,
+                                 int64_t D, int64_t d, int64_t T, double* state,
+                                 void* workspace, hipStream_t stream)
+{
+    (void)hipGetLastError();
+    if (T == 0) {
+        uint32_t g;
+        if (!blocks(B * D * 2 * d, &g)) return hipErrorInvalidConfiguration;
+        hipLaunchKernelGGL(companion_zero_kernel, dim3(g), dim3(kThreads), 0, stream, state,
+                           B * D * 2 * d);
+        return hipGetLastError();
+    }
+    double* gbuf = static_cast<double*>(workspace);
+    return bf16_io ? init_io<bf16>(a, u, B, D, d, T, state, gbuf, stream)
+                   : init_io<float>(a, u, B, D, d, T, state, gbuf, stream);
+}
+
+}  // namespace lh

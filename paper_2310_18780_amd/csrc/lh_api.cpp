@@ -11,6 +11,7 @@
 
 #include "lh_internal.hpp"
 #include "prefill_fft.hpp"
+#include "companion.hpp"
 
 namespace {
 
@@ -279,6 +280,126 @@ lh_status lh_prefill_fft(const lh_c32* lambda, const lh_c32* R, const float* h0,
                                D, d, T, reinterpret_cast<float2*>(state), y, plan, workspace,
                                static_cast<hipStream_t>(stream)),
         "FFT prefill launch");
+}
+
+lh_status lh_companion_coeffs(const lh_c32* lambda, const lh_c32* R, int64_t D, int64_t d,
+                              double* a, double* beta, void* stream)
+{
+    g_last_error[0] = '\0';
+    lh_status s;
+    if (!lambda || !R || !a || !beta)
+        return fail(LH_ERR_INVALID_ARG, "lambda, R, a and beta must not be NULL");
+    if (d < 1 || d > LH_COMPANION_MAX_MODES)
+        return fail(LH_ERR_INVALID_ARG, "d = %lld must be in [1, %d]", (long long)d,
+                    LH_COMPANION_MAX_MODES);
+    if ((s = check_sizes(1, D, d, 0)) != LH_OK) return s;
+    const Buf b_lam = buf("lambda", lambda, sizeof(lh_c32) * D * d);
+    const Buf b_R = buf("R", R, sizeof(lh_c32) * D * d);
+    const Buf b_a = buf("a", a, sizeof(double) * D * 2 * d);
+    const Buf b_beta = buf("beta", beta, sizeof(double) * D * 2 * d);
+    if ((s = check_align(b_lam, 8)) || (s = check_align(b_R, 8)) || (s = check_align(b_a, 8)) ||
+        (s = check_align(b_beta, 8)))
+        return s;
+    const Buf* ins[] = {&b_lam, &b_R};
+    const Buf* outs[] = {&b_a, &b_beta};
+    for (const Buf* o : outs)
+        for (const Buf* i : ins)
+            if (overlaps(*o, *i)) return fail(LH_ERR_OVERLAP, "%s overlaps %s", o->name, i->name);
+    if (overlaps(b_a, b_beta)) return fail(LH_ERR_OVERLAP, "a overlaps beta");
+    int dev = 0;
+    if ((s = check_device(&dev)) != LH_OK) return s;
+    for (const Buf* b : {&b_lam, &b_R, &b_a, &b_beta})
+        if ((s = check_accessible(*b, dev)) != LH_OK) return s;
+    return from_hip(lh::launch_companion_coeffs(reinterpret_cast<const float2*>(lambda),
+                                                reinterpret_cast<const float2*>(R), D, d, a, beta,
+                                                static_cast<hipStream_t>(stream)),
+                    "companion coefficients launch");
+}
+
+lh_status lh_companion_step(const double* a, const double* beta, const float* h0, double* state,
+                            const void* u_t, void* y_t, int64_t B, int64_t D, int64_t d,
+                            lh_dtype io_dtype, void* stream)
+{
+    g_last_error[0] = '\0';
+    lh_status s;
+    if (!a || !beta || !h0 || !state || !u_t || !y_t)
+        return fail(LH_ERR_INVALID_ARG, "a, beta, h0, state, u_t and y_t must not be NULL");
+    if (d < 1 || d > LH_COMPANION_MAX_MODES)
+        return fail(LH_ERR_INVALID_ARG, "d = %lld must be in [1, %d]", (long long)d,
+                    LH_COMPANION_MAX_MODES);
+    if ((s = check_sizes(B, D, d, 0)) != LH_OK) return s;
+    if ((s = check_dtype(io_dtype)) != LH_OK) return s;
+    const size_t es = io_dtype == LH_BF16 ? 2 : 4;
+    const Buf b_a = buf("a", a, sizeof(double) * D * 2 * d);
+    const Buf b_beta = buf("beta", beta, sizeof(double) * D * 2 * d);
+    const Buf b_h0 = buf("h0", h0, sizeof(float) * D);
+    const Buf b_state = buf("state", state, sizeof(double) * B * D * 2 * d);
+    const Buf b_u = buf("u_t", u_t, es * B * D);
+    const Buf b_y = buf("y_t", y_t, es * B * D);
+    if ((s = check_align(b_a, 8)) || (s = check_align(b_beta, 8)) || (s = check_align(b_h0, 4)) ||
+        (s = check_align(b_state, 16)) || (s = check_align(b_u, es)) || (s = check_align(b_y, es)))
+        return s;
+    const Buf* all[] = {&b_a, &b_beta, &b_h0, &b_state, &b_u, &b_y};
+    for (const Buf* o : {&b_state, &b_y})
+        for (const Buf* i : all)
+            if (o != i && overlaps(*o, *i))
+                return fail(LH_ERR_OVERLAP, "%s overlaps %s", o->name, i->name);
+    int dev = 0;
+    if ((s = check_device(&dev)) != LH_OK) return s;
+    for (const Buf* b : all)
+        if ((s = check_accessible(*b, dev)) != LH_OK) return s;
+    return from_hip(lh::launch_companion_step(a, beta, h0, state, u_t, y_t, io_dtype == LH_BF16,
+                                              B, D, d, static_cast<hipStream_t>(stream)),
+                    "companion step launch");
+}
+
+size_t lh_companion_init_workspace_bytes(int64_t D, int64_t d, int64_t T)
+{
+    if (d < 1 || d > LH_COMPANION_MAX_MODES || check_sizes(1, D, d, T) != LH_OK) return (size_t)-1;
+    return lh::companion_init_workspace_bytes(D, T);
+}
+
+lh_status lh_companion_init(const double* a, const void* u, int64_t B, int64_t D, int64_t d,
+                            int64_t T, lh_dtype io_dtype, double* state, void* workspace,
+                            size_t workspace_bytes, void* stream)
+{
+    g_last_error[0] = '\0';
+    lh_status s;
+    if (!a || !state) return fail(LH_ERR_INVALID_ARG, "a and state must not be NULL");
+    if (d < 1 || d > LH_COMPANION_MAX_MODES)
+        return fail(LH_ERR_INVALID_ARG, "d = %lld must be in [1, %d]", (long long)d,
+                    LH_COMPANION_MAX_MODES);
+    if ((s = check_sizes(B, D, d, T)) != LH_OK) return s;
+    if (T > 0 && !u) return fail(LH_ERR_INVALID_ARG, "u must not be NULL when T > 0");
+    if ((s = check_dtype(io_dtype)) != LH_OK) return s;
+    const size_t need = lh::companion_init_workspace_bytes(D, T);
+    const size_t es = io_dtype == LH_BF16 ? 2 : 4;
+    const Buf b_a = buf("a", a, sizeof(double) * D * 2 * d);
+    const Buf b_u = buf("u", u, T > 0 ? es * B * T * D : 0);
+    const Buf b_state = buf("state", state, sizeof(double) * B * D * 2 * d);
+    const Buf b_ws = buf("workspace", workspace, need);
+    if ((s = check_align(b_a, 8)) || (s = check_align(b_u, es)) || (s = check_align(b_state, 16)))
+        return s;
+    if (need > 0) {
+        if (!workspace)
+            return fail(LH_ERR_WORKSPACE, "workspace is NULL but %zu bytes are needed", need);
+        if (workspace_bytes < need)
+            return fail(LH_ERR_WORKSPACE, "workspace has %zu bytes, %zu are needed",
+                        workspace_bytes, need);
+        if ((s = check_align(b_ws, 256))) return s;
+    }
+    const Buf* ins[] = {&b_a, &b_u};
+    for (const Buf* o : {&b_state, &b_ws})
+        for (const Buf* i : ins)
+            if (overlaps(*o, *i)) return fail(LH_ERR_OVERLAP, "%s overlaps %s", o->name, i->name);
+    if (overlaps(b_state, b_ws)) return fail(LH_ERR_OVERLAP, "state overlaps workspace");
+    int dev = 0;
+    if ((s = check_device(&dev)) != LH_OK) return s;
+    for (const Buf* b : {&b_a, &b_u, &b_state, &b_ws})
+        if ((s = check_accessible(*b, dev)) != LH_OK) return s;
+    return from_hip(lh::launch_companion_init(a, u, io_dtype == LH_BF16, B, D, d, T, state,
+                                              workspace, static_cast<hipStream_t>(stream)),
+                    "companion initialisation launch");
 }
 
 lh_status lh_step(const lh_c32* lambda, const lh_c32* R, const float* h0, lh_c32* state,

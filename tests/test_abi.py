@@ -312,3 +312,75 @@ def test_prefill_fft_reports_no_device_without_gpu():
     assert L.lh_prefill_fft(*fft_args()) == 4
     assert L.lh_prefill_fft(*fft_args(io=lh.LH_BF16, B=3, d=7)) == 4
     assert L.lh_prefill_fft(*fft_args(T=0, u=None, y=None, ws=None, ws_bytes=0)) == 4
+
+
+def comp_coeff_args(**kw):
+    a = dict(lam=A, R=A + MB, D=8, d=4, a=A + 64 * MB, beta=A + 65 * MB, stream=None)
+    a.update(kw)
+    return [a[k] for k in ("lam", "R", "D", "d", "a", "beta", "stream")]
+
+
+def comp_step_args(**kw):
+    a = dict(a=A, beta=A + MB, h0=A + 2 * MB, state=A + 64 * MB, u=A + 3 * MB, y=A + 128 * MB,
+             B=2, D=8, d=4, io=lh.LH_F32, stream=None)
+    a.update(kw)
+    return [a[k] for k in ("a", "beta", "h0", "state", "u", "y", "B", "D", "d", "io", "stream")]
+
+
+def comp_init_args(**kw):
+    a = dict(a=A, u=A + 3 * MB, B=2, D=8, d=4, T=16, io=lh.LH_F32, state=A + 64 * MB,
+             ws=A + 256 * MB, ws_bytes=1 << 20, stream=None)
+    a.update(kw)
+    return [a[k] for k in ("a", "u", "B", "D", "d", "T", "io", "state", "ws", "ws_bytes", "stream")]
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(lam=None), 1), (dict(a=None), 1), (dict(beta=None), 1), (dict(D=0), 1), (dict(d=0), 1),
+    (dict(d=17), 1),                       # beyond LH_COMPANION_MAX_MODES
+    (dict(a=A + MB), 2),                   # a overlaps R
+    (dict(beta=A + 64 * MB + 64), 2),      # beta overlaps a
+    (dict(a=A + 64 * MB + 4), 1),          # misaligned float64
+])
+def test_companion_coeffs_rejects_bad_arguments(kw, status):
+    L = lh.lib()
+    assert L.lh_companion_coeffs(*comp_coeff_args(**kw)) == status
+    assert L.lh_last_error().decode() != ""
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(a=None), 1), (dict(state=None), 1), (dict(u=None), 1), (dict(y=None), 1),
+    (dict(B=0), 1), (dict(d=17), 1), (dict(io=4), 3),
+    (dict(state=A + 64 * MB + 8), 1),      # state must be 16-byte aligned
+    (dict(y=A + 3 * MB), 2),               # y_t aliases u_t
+    (dict(state=A + MB), 2),               # state overlaps beta
+])
+def test_companion_step_rejects_bad_arguments(kw, status):
+    L = lh.lib()
+    assert L.lh_companion_step(*comp_step_args(**kw)) == status
+    assert L.lh_last_error().decode() != ""
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(a=None), 1), (dict(state=None), 1), (dict(u=None), 1), (dict(T=-1), 1), (dict(d=17), 1),
+    (dict(io=9), 3), (dict(ws=None), 5), (dict(ws_bytes=8), 5),
+    (dict(ws=A + 256 * MB + 8), 1),        # misaligned workspace
+    (dict(state=A + 3 * MB), 2),           # state overlaps u
+    (dict(ws=A + 64 * MB), 2),             # workspace overlaps state
+])
+def test_companion_init_rejects_bad_arguments(kw, status):
+    L = lh.lib()
+    assert L.lh_companion_init(*comp_init_args(**kw)) == status
+    assert L.lh_last_error().decode() != ""
+
+
+def test_companion_workspace_and_no_device():
+    assert lh.companion_init_workspace_bytes(8, 4, 0) == 0
+    assert lh.companion_init_workspace_bytes(8, 4, 16) == 16 * 8 * 8
+    assert lh.lib().lh_companion_init_workspace_bytes(8, 17, 16) == ctypes.c_size_t(-1).value
+    if not no_gpu():
+        pytest.skip("made-up addresses are only passed through when no GPU is visible")
+    L = lh.lib()
+    assert L.lh_companion_coeffs(*comp_coeff_args()) == 4
+    assert L.lh_companion_step(*comp_step_args()) == 4
+    assert L.lh_companion_init(*comp_init_args()) == 4
+    assert L.lh_companion_init(*comp_init_args(T=0, u=None, ws=None, ws_bytes=0)) == 4
