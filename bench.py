@@ -54,6 +54,10 @@ def parse():
                    help="time the FFT prefill (lh_prefill_fft) beside the scan prefill on "
                         "--fft-workload")
     p.add_argument("--fft-workload", default="c5")
+    p.add_argument("--companion", action="store_true",
+                   help="time the companion-form decode step and fast initialisation beside the "
+                        "modal ones on --companion-workload")
+    p.add_argument("--companion-workload", default="cp")
     p.add_argument("--distill", action="store_true",
                    help="time the distillation objective (lh_distill) on --workload's filter "
                         "bank with L = its T")
@@ -495,6 +499,123 @@ def fft_main(args):
     print(json.dumps(out), flush=True)
 
 
+def companion_step_bytes(w):
+    """Algorithmic bytes of one companion step: the float64 state [B, D, 2d]
+    read and written, u_t and y_t, the coefficients a, beta [D, 2d] and h0."""
+    es = 2 if w.io == "bf16" else 4
+    return 2 * 8 * w.B * w.D * 2 * w.d + 2 * es * w.B * w.D + 2 * 8 * w.D * 2 * w.d + 4 * w.D
+
+
+def companion_main(args):
+    import numpy as np
+    import torch
+
+    import paper_2310_18780_amd as lh
+    import workloads
+
+    lh.lib()
+    w = workloads.workload(args.companion_workload)
+    t = make_device_inputs(w)
+    B, T, D, d, K = w.B, w.T, w.D, w.d, w.K
+    a = torch.empty((D, 2 * d), dtype=torch.float64, device="cuda")
+    beta = torch.empty_like(a)
+    xc = torch.empty((B, D, 2 * d), dtype=torch.float64, device="cuda")
+    xm = torch.empty((B, D, d), dtype=torch.complex64, device="cuda")
+    ws = torch.empty(max(lh.companion_init_workspace_bytes(D, d, T), 1), dtype=torch.uint8,
+                     device="cuda")
+    y_dec = torch.empty((K, B, D), dtype=t["u"].dtype, device="cuda")
+    stream = torch.cuda.current_stream()
+    ev = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
+
+    def timed(fn, reps):
+        fn()
+        torch.cuda.synchronize()
+        s, e = ev(), ev()
+        s.record(stream)
+        for _ in range(reps):
+            fn()
+        e.record(stream)
+        torch.cuda.synchronize()
+        return s.elapsed_time(e) / reps
+
+    coeff_ms = timed(lambda: lh.companion_coeffs(t["lam"], t["R"], a, beta), 5)
+    init_ms = timed(lambda: lh.companion_init(a, t["u"], xc, workspace=ws), max(3, args.steps // 4))
+
+    def graph_of(step):
+        step()
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            step()
+        return g
+
+    gc = graph_of(lambda: [lh.companion_step(a, beta, t["h0"], xc, t["ud"][k], y_dec[k])
+                           for k in range(K)])
+    gm = graph_of(lambda: [lh.step(t["lam"], t["R"], t["h0"], xm, t["ud"][k], y_dec[k])
+                           for k in range(K)])
+    for _ in range(args.warmup):
+        gc.replay()
+        gm.replay()
+    t0 = time.perf_counter()
+    comp_ms = timed(gc.replay, args.steps)
+    wall = (time.perf_counter() - t0) * 1e3 / args.steps
+    modal_ms = timed(gm.replay, args.steps)
+    us = comp_ms * 1e3 / K
+    nbytes = companion_step_bytes(w)
+    gbs = nbytes / (us * 1e-6) / 1e9
+    cpu = None
+    if not args.no_cpu_baseline:
+        import oracle
+        import oracle.companion as oc
+
+        lam, R, h0 = workloads.make_params(w)
+        ar, br, b0 = oc.from_modal(lam, R, h0)
+        done, t1 = 0, time.perf_counter()
+        x0 = np.zeros(2 * d)
+        for b in range(B):
+            ud = workloads.decode_row(w, b)
+            for c in range(D):
+                oc.companion_run(ar[c], br[c], b0[c], ud[:, c], x0)
+                done += 1
+                if time.perf_counter() - t1 > 10.0:
+                    break
+            if time.perf_counter() - t1 > 10.0:
+                break
+        dt = time.perf_counter() - t1
+        cpu = {"value": done / D * K / dt, "unit": "tokens/s", "cores": 1, "kind": "oracle",
+               "sample": f"{done} (b,c) rows of {w.name}, K={K} companion steps each (float64 "
+                         f"numpy, one process) in {dt:.2f} s; value = steps per second scaled "
+                         f"to whole sequences (rows / D * K / time)",
+               "seconds": dt}
+    out = {
+        "metric": "decode tokens/s (companion-form recurrence)",
+        "value": B * K / (comp_ms * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": wall,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f64",
+        "data": "synthetic",
+        "config": {"workload": w.name, "B": B, "D": D, "d": d, "order": 2 * d, "T": T, "K": K,
+                   "io": w.io},
+        "companion_us_per_token_step": us,
+        "modal_us_per_token_step": modal_ms * 1e3 / K,
+        "modal_tokens_per_s": B * K / (modal_ms * 1e-3),
+        "init_ms": init_ms,
+        "init_tokens_per_s": B * T / (init_ms * 1e-3),
+        "coeffs_ms": coeff_ms,
+        "roofline": {"bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": gbs / HBM_PEAK_GBS, "traffic": None,
+                     "kernel": "companion_step_kernel", "bytes_per_launch": nbytes},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -513,6 +634,9 @@ def main():
         return
     if args.fft:
         fft_main(args)
+        return
+    if args.companion:
+        companion_main(args)
         return
 
     import torch

@@ -228,7 +228,8 @@ lh_status lh_companion_coeffs(const lh_c32* lambda, const lh_c32* R, int64_t D, 
  *                    state[b,c,2d-2])                               (in place)
  * in float64, y_t rounded to io_dtype.
  *
- *   a, beta : [D, 2d] float64 (lh_companion_coeffs);  h0 : [D] float32
+ *   a, beta : [D, 2d] float64 (lh_companion_coeffs), 16-byte aligned
+ *   h0      : [D] float32
  *   state   : in/out [B, D, 2d] float64, 16-byte aligned
  *   u_t, y_t: [B, D] (io_dtype)
  * y_t must not overlap any other buffer; state must not overlap a, beta, h0

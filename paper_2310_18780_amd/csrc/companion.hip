@@ -33,6 +33,7 @@ namespace {
 
 constexpr int kMaxOrd = 2 * kCompanionMaxModes;
 constexpr int kThreads = 256;
+constexpr int kBlk = 8;  // initialisation: steps per prefetched block
 
 // One 64-thread workgroup per channel; thread k owns the coefficient of w^k.
 __global__ __launch_bounds__(64) void companion_coeffs_kernel(const float2* __restrict__ lam,
@@ -88,38 +89,46 @@ __global__ __launch_bounds__(64) void companion_coeffs_kernel(const float2* __re
     }
 }
 
-// One thread per (b, c) row; the row's 2d state entries in registers.
+// G = 2^k >= d lanes per (b, c) row, lane j holding the state pair
+// (x[2j], x[2j+1]) (16 bytes: a wave moves contiguous kilobytes).  The two
+// dot products are reduced over the row's lanes with butterfly shuffles; the
+// shift takes x[2j-1] from the lane below.
+constexpr int next_pow2(int x) { return x <= 1 ? 1 : 2 * next_pow2((x + 1) / 2); }
+
 template <typename IO, int ORD>
 __global__ __launch_bounds__(kThreads) void companion_step_kernel(
     const double* __restrict__ a, const double* __restrict__ beta, const float* __restrict__ h0,
     double* __restrict__ state, const IO* __restrict__ u, IO* __restrict__ y, int64_t B,
     int64_t D)
 {
-    const int64_t i = int64_t(blockIdx.x) * kThreads + threadIdx.x;
-    if (i >= B * D) return;
-    const int64_t c = i % D;
-    double2* xs = reinterpret_cast<double2*>(state + i * ORD);
-    double x[ORD];
-#pragma unroll
-    for (int m = 0; m < ORD / 2; ++m) {
-        const double2 v = xs[m];
-        x[2 * m] = v.x;
-        x[2 * m + 1] = v.y;
+    constexpr int P = ORD / 2;           // state pairs per row
+    constexpr int G = next_pow2(P);      // lanes per row
+    const int64_t gid = int64_t(blockIdx.x) * kThreads + threadIdx.x;
+    const int64_t row = gid / G;         // b * D + c
+    const int j = static_cast<int>(gid % G);
+    const bool live = row < B * D;       // whole groups leave together: no exits before shuffles
+    const int64_t rr = live ? row : 0;
+    const int64_t c = rr % D;
+    const bool own = live && j < P;
+    double2 x = make_double2(0.0, 0.0), av = x, bv = x;
+    if (own) {
+        x = reinterpret_cast<const double2*>(state + rr * ORD)[j];
+        av = reinterpret_cast<const double2*>(a + c * ORD)[j];
+        bv = reinterpret_cast<const double2*>(beta + c * ORD)[j];
     }
-    const double* ac = a + c * ORD;
-    const double* bc = beta + c * ORD;
-    const double ut = io_load(u + i);
-    double out = 0.0, fb = 0.0;
+    double out = fma(bv.x, x.x, bv.y * x.y);
+    double fb = fma(av.x, x.x, av.y * x.y);
 #pragma unroll
-    for (int m = 0; m < ORD; ++m) {
-        out = fma(bc[m], x[m], out);
-        fb = fma(ac[m], x[m], fb);
+    for (int m = 1; m < G; m *= 2) {
+        out += __shfl_xor(out, m, G);
+        fb += __shfl_xor(fb, m, G);
     }
-    out = fma(static_cast<double>(h0[c]), ut, out);
-    io_store(y + i, static_cast<float>(out));
-    xs[0] = make_double2(ut - fb, x[0]);
-#pragma unroll
-    for (int m = 1; m < ORD / 2; ++m) xs[m] = make_double2(x[2 * m - 1], x[2 * m]);
+    const double below = __shfl_up(x.y, 1, G);  // x[2j-1]
+    if (!own) return;
+    const double ut = io_load(u + rr);
+    if (j == 0) io_store(y + rr, static_cast<float>(fma(static_cast<double>(h0[c]), ut, out)));
+    reinterpret_cast<double2*>(state + rr * ORD)[j] =
+        make_double2(j == 0 ? ut - fb : below, x.x);
 }
 
 // g_t for t < T per channel (one thread per channel): g_0 = 1,
@@ -166,15 +175,48 @@ __global__ __launch_bounds__(kThreads) void companion_init_kernel(const double* 
         win[j] = T - 1 - j >= 0 ? g[(T - 1 - j) * D + c] : 0.0;
         acc[j] = 0.0;
     }
-    for (int64_t k = 0; k < T; ++k) {
-        const double uk = io_load(ub + k * D);
+    // one step k: accumulate, then slide the window (next tap g_{T-1-2d-k})
+    auto step = [&](double uk, double gnext) {
 #pragma unroll
         for (int j = 0; j < ORD; ++j) acc[j] = fma(win[j], uk, acc[j]);
 #pragma unroll
         for (int j = 0; j < ORD - 1; ++j) win[j] = win[j + 1];
-        const int64_t nx = T - 1 - ORD - k;
-        win[ORD - 1] = nx >= 0 ? g[nx * D + c] : 0.0;
+        win[ORD - 1] = gnext;
+    };
+    auto gtap = [&](int64_t k) { return T - 1 - ORD - k >= 0 ? g[(T - 1 - ORD - k) * D + c] : 0.0; };
+    // blocks of kBlk steps, the next block's inputs loaded while the current
+    // one is used (two buffers in turn), then the remaining steps
+    const int64_t nblk = T / kBlk;
+    double ua[kBlk], ga[kBlk], ub2[kBlk], gb[kBlk];
+    auto load = [&](double (&uu)[kBlk], double (&gg)[kBlk], int64_t k0) {
+#pragma unroll
+        for (int s2 = 0; s2 < kBlk; ++s2) {
+            uu[s2] = io_load(ub + (k0 + s2) * D);
+            gg[s2] = gtap(k0 + s2);
+        }
+        // keep the loads here, ahead of the arithmetic that follows
+        asm volatile("" ::: "memory");
+        __builtin_amdgcn_sched_barrier(0);
+    };
+    auto use = [&](const double (&uu)[kBlk], const double (&gg)[kBlk]) {
+#pragma unroll
+        for (int s2 = 0; s2 < kBlk; ++s2) step(uu[s2], gg[s2]);
+    };
+    int64_t k = 0;
+    if (nblk > 0) {
+        load(ua, ga, 0);
+        for (int64_t blk = 0; blk < nblk; blk += 2) {
+            const bool more1 = blk + 1 < nblk, more2 = blk + 2 < nblk;
+            load(ub2, gb, more1 ? k + kBlk : k);  // past the last block: reload (unused)
+            use(ua, ga);
+            k += kBlk;
+            if (!more1) break;
+            load(ua, ga, more2 ? k + kBlk : k);
+            use(ub2, gb);
+            k += kBlk;
+        }
     }
+    for (; k < T; ++k) step(io_load(ub + k * D), gtap(k));
     double2* xs = reinterpret_cast<double2*>(state + i * ORD);
 #pragma unroll
     for (int m = 0; m < ORD / 2; ++m) xs[m] = make_double2(acc[2 * m], acc[2 * m + 1]);
@@ -203,7 +245,7 @@ hipError_t step_io(const double* a, const double* beta, const float* h0, double*
                    const void* u_t, void* y_t, int64_t B, int64_t D, int64_t d, hipStream_t s)
 {
     uint32_t g;
-    if (!blocks(B * D, &g)) return hipErrorInvalidConfiguration;
+    if (!blocks(B * D * next_pow2(static_cast<int>(d)), &g)) return hipErrorInvalidConfiguration;
     switch (2 * d) {
 #define LH_CASE(O)                                                                              \
     case O:                                                                                     \

@@ -336,7 +336,7 @@ lh_status lh_companion_step(const double* a, const double* beta, const float* h0
     const Buf b_state = buf("state", state, sizeof(double) * B * D * 2 * d);
     const Buf b_u = buf("u_t", u_t, es * B * D);
     const Buf b_y = buf("y_t", y_t, es * B * D);
-    if ((s = check_align(b_a, 8)) || (s = check_align(b_beta, 8)) || (s = check_align(b_h0, 4)) ||
+    if ((s = check_align(b_a, 16)) || (s = check_align(b_beta, 16)) || (s = check_align(b_h0, 4)) ||
         (s = check_align(b_state, 16)) || (s = check_align(b_u, es)) || (s = check_align(b_y, es)))
         return s;
     const Buf* all[] = {&b_a, &b_beta, &b_h0, &b_state, &b_u, &b_y};

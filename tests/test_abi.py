@@ -351,6 +351,7 @@ def test_companion_coeffs_rejects_bad_arguments(kw, status):
     (dict(a=None), 1), (dict(state=None), 1), (dict(u=None), 1), (dict(y=None), 1),
     (dict(B=0), 1), (dict(d=17), 1), (dict(io=4), 3),
     (dict(state=A + 64 * MB + 8), 1),      # state must be 16-byte aligned
+    (dict(beta=A + MB + 8), 1),            # so must the coefficients
     (dict(y=A + 3 * MB), 2),               # y_t aliases u_t
     (dict(state=A + MB), 2),               # state overlaps beta
 ])

@@ -91,6 +91,9 @@ WORKLOADS: Dict[str, Workload] = {
         Workload("b64_d2048_n16_t4096_bf16", 64, 2048, 16, 4096, 512, "bf16", 0.9, 0.9999, math.pi, 1.0 / 16),
         Workload("b256_d2048_n64_t1024", 256, 2048, 64, 1024, 1024, "f32", 0.9, 0.9999, math.pi, 1.0 / 64),
         Workload("b4_d1024_n32_t65536", 4, 1024, 32, 65536, 128, "f32", 0.999, 0.99999, 0.01 * math.pi, 1.0 / 32),
+        # the companion form's workload: an order (2d = 16) and pole radii at which
+        # its float64 recurrence keeps the modal path's accuracy
+        Workload("cp_b256_d2048_n8_t1024", 256, 2048, 8, 1024, 64, "f32", 0.8, 0.99, math.pi, 1.0 / 8),
     )
 }
 
@@ -102,6 +105,7 @@ ALIASES = {
     "c3": "b64_d2048_n16_t4096_bf16",
     "c4": "b256_d2048_n64_t1024",
     "c5": "b4_d1024_n32_t65536",
+    "cp": "cp_b256_d2048_n8_t1024",
 }
 
 
