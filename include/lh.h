@@ -82,8 +82,9 @@ typedef enum lh_status {
 /* Largest supported number of modes per channel. */
 #define LH_MAX_MODES 1024
 
-/* chunk_len value that requests the matrix-core prefill plan (see lh_prefill). */
+/* chunk_len values that request the matrix-core prefill plans (see lh_prefill). */
 #define LH_PREFILL_MFMA (-1)
+#define LH_PREFILL_MFMA_SEG (-2)
 
 /* LH_ABI_VERSION of the built library. */
 int lh_abi_version(void);
@@ -126,7 +127,18 @@ size_t lh_prefill_workspace_bytes(int64_t B, int64_t D, int64_t d, int64_t T,
  *                   LH_ERR_INVALID_ARG).  The automatic plan uses the matrix
  *                   cores where supported and ceil(D/16) * ceil(B/32) >= 256
  *                   (enough workgroups to fill the GPU without splitting the
- *                   prompt in time)
+ *                   prompt in time);
+ *                   LH_PREFILL_MFMA_SEG = the segmented matrix-core plan: the
+ *                   prompt is cut into 2^k segments of T / 2^k steps (a
+ *                   multiple of 32, at least 256), the fewest whose (batch
+ *                   row, segment) pairs fill the GPU; a matrix-core pass
+ *                   computes each segment's end state from zero, a carry
+ *                   gives each segment its entry state, and a second
+ *                   matrix-core pass computes the outputs (same operand
+ *                   splitting and requirements as LH_PREFILL_MFMA, and such a
+ *                   T).  The automatic plan takes it where the whole-prompt
+ *                   matrix-core plan is supported but not chosen and T splits
+ *                   this way
  *   workspace     : device scratch of at least
  *                   lh_prefill_workspace_bytes(B,D,d,T,chunk_len) bytes,
  *                   256-byte aligned; may be NULL when that size is 0.  Its

@@ -202,7 +202,7 @@ const char* lh_last_error(void) { return g_last_error; }
 
 size_t lh_prefill_workspace_bytes(int64_t B, int64_t D, int64_t d, int64_t T, int64_t chunk_len)
 {
-    if (check_sizes(B, D, d, T) != LH_OK || chunk_len < LH_PREFILL_MFMA) return (size_t)-1;
+    if (check_sizes(B, D, d, T) != LH_OK || chunk_len < LH_PREFILL_MFMA_SEG) return (size_t)-1;
     lh::PrefillPlan p;
     if (!lh::make_prefill_plan(B, D, d, T, chunk_len, &p)) return (size_t)-1;
     return p.ws_bytes;
@@ -219,14 +219,18 @@ lh_status lh_prefill(const lh_c32* lambda, const lh_c32* R, const float* h0, con
         return fail(LH_ERR_INVALID_ARG, "lambda, R, h0 and state must not be NULL");
     if ((s = check_sizes(B, D, d, T)) != LH_OK) return s;
     if (T > 0 && (!u || !y)) return fail(LH_ERR_INVALID_ARG, "u and y must not be NULL when T > 0");
-    if (chunk_len < LH_PREFILL_MFMA)
-        return fail(LH_ERR_INVALID_ARG, "chunk_len must be >= 0 or LH_PREFILL_MFMA");
+    if (chunk_len < LH_PREFILL_MFMA_SEG)
+        return fail(LH_ERR_INVALID_ARG,
+                    "chunk_len must be >= 0, LH_PREFILL_MFMA or LH_PREFILL_MFMA_SEG");
     if ((s = check_dtype(io_dtype)) != LH_OK) return s;
     lh::PrefillPlan plan;
     if (!lh::make_prefill_plan(B, D, d, T, chunk_len, &plan))
         return fail(LH_ERR_INVALID_ARG, "no prefill plan for these sizes%s",
                     chunk_len == LH_PREFILL_MFMA
                         ? " (the matrix-core plan needs d = 16 or 32, D % 8 == 0, T >= 1)"
+                    : chunk_len == LH_PREFILL_MFMA_SEG
+                        ? " (the segmented matrix-core plan also needs T = s * 2^k * 32 "
+                          "steps, k >= 1, segments of at least 256 steps)"
                         : "");
     if (plan.mfma_forced && (reinterpret_cast<uintptr_t>(u) % 16 != 0 ||
                              reinterpret_cast<uintptr_t>(y) % 16 != 0))

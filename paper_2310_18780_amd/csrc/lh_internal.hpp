@@ -43,6 +43,12 @@ struct PrefillPlan {
     bool mfma;        // matrix-core prefill (automatic plans use it when u and y are
                       // 16-byte aligned, else the VALU plan above)
     bool mfma_forced; // requested explicitly: u and y must be 16-byte aligned
+    bool mfma_seg;    // segmented matrix-core plan: the prompt is cut into nchunks
+                      // segments of C steps (C % 32 == 0, T == nchunks C); state pass
+                      // and output pass on the matrix cores, carry in between (falls
+                      // back to the VALU chunked scan with the same C when u or y is
+                      // not 16-byte aligned)
+    size_t off_mfma;  // workspace offset of the matrix-core tables (segmented plan)
 };
 
 // Returns false when the sizes are invalid or overflow.
@@ -59,6 +65,18 @@ hipError_t launch_prefill(const float2* lam, const float2* R, const float* h0,
 bool mfma_supported(int64_t B, int64_t D, int64_t d, int64_t T);
 bool mfma_preferred(int64_t B, int64_t D, int64_t d);
 size_t mfma_workspace_bytes(int64_t D, int64_t d);
+// Segment count of the segmented matrix-core plan (0 when T does not split
+// into segments of a multiple of 32 steps, at least 256 long).
+int64_t mfma_segments(int64_t B, int64_t D, int64_t T);
+hipError_t launch_mfma_setup(const float2* lam, const float2* R, const float* h0, int64_t D,
+                             int64_t d, void* workspace, hipStream_t stream);
+// One pass of the segmented plan: outputs = false writes each segment's end
+// state from zero into slot k < nseg - 1 of xs [B, nseg, D, d]; outputs = true
+// runs every segment from its entry state in xs, writes y and x_T.
+hipError_t launch_mfma_segment_pass(bool outputs, const float2* lam, const void* u,
+                                    bool bf16_io, int64_t B, int64_t D, int64_t d, int64_t T,
+                                    int nseg, int64_t seg_len, float2* xs, float2* state,
+                                    void* y, const void* workspace, hipStream_t stream);
 hipError_t launch_prefill_mfma(const float2* lam, const float2* R, const float* h0,
                                const void* u, bool bf16_io, int64_t B, int64_t D, int64_t d,
                                int64_t T, float2* state, void* y, void* workspace,

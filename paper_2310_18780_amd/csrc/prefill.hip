@@ -290,7 +290,7 @@ inline bool grid_for(int64_t n, dim3* g)
 bool make_prefill_plan(int64_t B, int64_t D, int64_t d, int64_t T, int64_t chunk_len,
                        PrefillPlan* plan)
 {
-    if (B < 1 || D < 1 || d < 1 || d > 1024 || T < 0 || chunk_len < -1) return false;
+    if (B < 1 || D < 1 || d < 1 || d > 1024 || T < 0 || chunk_len < -2) return false;
     // element counts must fit comfortably in int64 (and the byte sizes too)
     const int64_t lim = INT64_C(1) << 58;
     if (B > lim / D || B * D > lim / (T > d ? (T > 0 ? T : 1) : d)) return false;
@@ -340,13 +340,33 @@ bool make_prefill_plan(int64_t B, int64_t D, int64_t d, int64_t T, int64_t chunk
     // The automatic plan runs on the matrix cores where supported; the
     // workspace also covers the VALU plan above, taken when u or y is not
     // 16-byte aligned.
-    p.mfma_forced = chunk_len == -1;
+    p.mfma_forced = chunk_len == -1 || chunk_len == -2;
     if (p.mfma_forced && !mfma_supported(B, D, d, T)) return false;
-    p.mfma = p.mfma_forced ||
+    p.mfma = chunk_len == -1 ||
              (chunk_len == 0 && mfma_supported(B, D, d, T) && mfma_preferred(B, D, d));
+    p.mfma_seg = false;
+    p.off_mfma = 0;
     if (p.mfma) {
         const size_t mb = mfma_workspace_bytes(D, d);
         if (p.mfma_forced || mb > p.ws_bytes) p.ws_bytes = mb;  // a forced plan has no fallback
+    } else if ((chunk_len == 0 || chunk_len == -2) && mfma_supported(B, D, d, T)) {
+        // too few (batch row, channel group) tiles for the whole-prompt matrix-core
+        // plan: cut the prompt into segments that run in parallel, on the matrix
+        // cores, with the chunked scan's carry in between
+        const int64_t nseg = mfma_segments(B, D, T);
+        if (nseg >= 2) {
+            p.mfma_seg = true;
+            p.C = T / nseg;
+            p.nchunks = nseg;
+            const size_t pow_bytes = static_cast<size_t>(D) * d * sizeof(float2);
+            p.off_pow = 0;
+            p.off_xin = (pow_bytes + 255) / 256 * 256;
+            const size_t xin_bytes = static_cast<size_t>(B) * nseg * D * d * sizeof(float2);
+            p.off_mfma = (p.off_xin + xin_bytes + 255) / 256 * 256;
+            p.ws_bytes = p.off_mfma + mfma_workspace_bytes(D, d);
+        } else if (chunk_len == -2) {
+            return false;
+        }
     }
     *plan = p;
     return true;
@@ -370,6 +390,24 @@ hipError_t launch_prefill(const float2* lam, const float2* R, const float* h0, c
     if (p.mfma && aligned16)
         return launch_prefill_mfma(lam, R, h0, u, bf16_io, B, D, d, T, state, y, workspace,
                                    stream);
+    if (p.mfma_seg && aligned16) {
+        char* ws = static_cast<char*>(workspace);
+        float2* lamC = reinterpret_cast<float2*>(ws + p.off_pow);
+        float2* xs = reinterpret_cast<float2*>(ws + p.off_xin);
+        void* mws = ws + p.off_mfma;
+        hipError_t e;
+        hipLaunchKernelGGL(pow_kernel, g_pow, dim3(kBlock), 0, stream, lam, lamC, D * d, p.C);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        if ((e = launch_mfma_setup(lam, R, h0, D, d, mws, stream)) != hipSuccess) return e;
+        if ((e = launch_mfma_segment_pass(false, lam, u, bf16_io, B, D, d, T, int(p.nchunks), p.C,
+                                          xs, state, y, mws, stream)) != hipSuccess)
+            return e;
+        hipLaunchKernelGGL(carry_kernel, g_state, dim3(kBlock), 0, stream, lamC, xs, B, D * d,
+                           p.nchunks);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        return launch_mfma_segment_pass(true, lam, u, bf16_io, B, D, d, T, int(p.nchunks), p.C,
+                                        xs, state, y, mws, stream);
+    }
     float2* lamC = nullptr;
     float2* xs = nullptr;
     hipError_t e;

@@ -231,11 +231,23 @@ struct Stage<float> {
     static constexpr int kNTA = kTerms;
 };
 
-template <typename IO, int DM, int NBG>
+// MODE selects what a column of the MFMA tiles is:
+//   kWhole    : a batch row over the whole prompt, from x = 0; writes y and x_T;
+//   kSegState : a (batch row b, segment k < nseg - 1) pair over the seg_len steps
+//               of segment k, from x = 0; writes only its end state s_k to
+//               xs[b][k] (no outputs);
+//   kSegOut   : a (b, k < nseg) pair from the entry state xs[b][k] (the carry
+//               of the earlier segments); writes y over the segment, and x_T
+//               for the last segment.
+// Segmented launches need seg_len % C == 0 and T == nseg seg_len.
+enum { kWhole = 0, kSegState = 1, kSegOut = 2 };
+
+template <typename IO, int DM, int NBG, int MODE>
 __global__ __launch_bounds__(kThreads) void mfma_prefill_kernel(
     const float2* __restrict__ lam, const IO* __restrict__ u, IO* __restrict__ y,
     float2* __restrict__ state, const bf16x8* __restrict__ frag,
-    const float2* __restrict__ lamc, int B, int D, int64_t T, int ncg, int nbg, int per_xcd)
+    const float2* __restrict__ lamc, int B, int D, int64_t T, int ncg, int nbg, int per_xcd,
+    int nseg, int64_t seg_len, float2* __restrict__ xs)
 {
     constexpr int d = 16 * DM;
     constexpr int F = n_frag(DM);
@@ -272,6 +284,13 @@ __global__ __launch_bounds__(kThreads) void mfma_prefill_kernel(
     if (bgw >= nbg) return;  // whole workgroup exits together
     const int c0 = cg * CW;
     const int b0 = bgw * BN;
+    // columns ("rows" below): batch rows, or (batch row, segment) pairs
+    // r = b * SV + k, each covering TL steps from time TB(r)
+    const int SV = MODE == kWhole ? 1 : MODE == kSegState ? nseg - 1 : nseg;
+    const int BV = B * SV;
+    const int64_t TL = MODE == kWhole ? T : seg_len;
+    auto row_b = [&](int r) { return r / SV; };
+    auto row_k = [&](int r) { return r % SV; };
 
     const int tid = threadIdx.x;
     const int w = tid / 64, lane = tid % 64;
@@ -298,11 +317,26 @@ __global__ __launch_bounds__(kThreads) void mfma_prefill_kernel(
 #pragma unroll
     for (int k = 0; k < CPW; ++k)
 #pragma unroll
-        for (int bg = 0; bg < NBG; ++bg)
+        for (int bg = 0; bg < NBG; ++bg) {
 #pragma unroll
             for (int mt = 0; mt < 2 * DM; ++mt) X[k][bg][mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+            if constexpr (MODE == kSegOut) {  // entry state of the segment
+                const int r = min(b0 + kN * bg + n, BV - 1);
+                const int cc = min(c0 + w * CPW + k, D - 1);
+                const float2* src =
+                    xs + ((int64_t(row_b(r)) * nseg + row_k(r)) * D + cc) * d;
+#pragma unroll
+                for (int q = 0; q < DM; ++q)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        const float2 v = src[16 * q + 4 * g + i];
+                        X[k][bg][q][i] = v.x;
+                        X[k][bg][DM + q][i] = v.y;
+                    }
+            }
+        }
 
-    const int64_t nch = (T + kC - 1) / kC;
+    const int64_t nch = (TL + kC - 1) / kC;
 
     // ---- u staging: item p = tid + j kThreads holds (row p / (16 PPR), steps
     // 2 ((p / PPR) % 16) + {0, 1}, channels c0 + CPP (p % PPR) ..).  Loads are
@@ -320,12 +354,13 @@ __global__ __launch_bounds__(kThreads) void mfma_prefill_kernel(
     for (int j = 0; j < IPT; ++j) {
         int ip, itp, irb;
         item_of(j, ip, itp, irb);
-        src0[j] = u + (int64_t(min(b0 + irb, B - 1)) * T + 2 * itp) * D +
+        const int r = min(b0 + irb, BV - 1);
+        src0[j] = u + (int64_t(row_b(r)) * T + int64_t(row_k(r)) * TL + 2 * itp) * D +
                   min(c0 + ip * CPP, D - CPP);
     }
     uint4 R0[IPT][2];
     auto load_tile = [&](int64_t kk) {
-        if ((kk + 1) * kC <= T) {  // full chunk (uniform branch)
+        if ((kk + 1) * kC <= TL) {  // full chunk (uniform branch)
             const int64_t off = kk * kC * D;
 #pragma unroll
             for (int j = 0; j < IPT; ++j)
@@ -340,7 +375,7 @@ __global__ __launch_bounds__(kThreads) void mfma_prefill_kernel(
 #pragma unroll
                 for (int h = 0; h < 2; ++h) {
                     const int64_t t = kk * kC + 2 * itp + h;
-                    const int64_t tc = (t < T ? t : T - 1) - 2 * itp;
+                    const int64_t tc = (t < TL ? t : TL - 1) - 2 * itp;
                     R0[j][h] = *reinterpret_cast<const uint4*>(src0[j] + tc * D);
                 }
             }
@@ -352,9 +387,9 @@ __global__ __launch_bounds__(kThreads) void mfma_prefill_kernel(
             if (tid + j * kThreads >= NITEM) continue;
             int ip, itp, irb;
             item_of(j, ip, itp, irb);
-            const bool in = b0 + irb < B && c0 + ip * CPP < D;
-            const bool ok0 = in && kk * kC + 2 * itp < T;
-            const bool ok1 = in && kk * kC + 2 * itp + 1 < T;
+            const bool in = b0 + irb < BV && c0 + ip * CPP < D;
+            const bool ok0 = in && kk * kC + 2 * itp < TL;
+            const bool ok1 = in && kk * kC + 2 * itp + 1 < TL;
 #pragma unroll
             for (int ch = 0; ch < CPP; ++ch) {
                 const int e = ((ip * CPP + ch) * BN + irb) * US + 2 * itp;  // element of step 2 itp
@@ -447,7 +482,7 @@ __global__ __launch_bounds__(kThreads) void mfma_prefill_kernel(
 #pragma unroll
             for (int k = 0; k < CPW; ++k) {
                 load_u(k, bg, U[k]);
-                split_x(X[k][bg], XB[k]);
+                if constexpr (MODE != kSegState) split_x(X[k][bg], XB[k]);
                 Y[k][0] = Y[k][1] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
                 for (int q = 0; q < DM; ++q) Sr[k][q] = Si[k][q] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -459,9 +494,11 @@ __global__ __launch_bounds__(kThreads) void mfma_prefill_kernel(
                     if (ia + ju >= KT) continue;
 #pragma unroll
                     for (int k = 0; k < CPW; ++k) {
+                        if constexpr (MODE != kSegState) {
 #pragma unroll
-                        for (int mt = 0; mt < 2; ++mt)
-                            Y[k][mt] = mfma(A[k][2 * DM + mt][ia], U[k][ju], Y[k][mt]);
+                            for (int mt = 0; mt < 2; ++mt)
+                                Y[k][mt] = mfma(A[k][2 * DM + mt][ia], U[k][ju], Y[k][mt]);
+                        }
 #pragma unroll
                         for (int q = 0; q < DM; ++q) {
                             Sr[k][q] = mfma(A[k][q][ia], U[k][ju], Sr[k][q]);
@@ -469,16 +506,18 @@ __global__ __launch_bounds__(kThreads) void mfma_prefill_kernel(
                         }
                     }
                 }
+            if constexpr (MODE != kSegState) {
 #pragma unroll
-            for (int p = 0; p < kWX; ++p)
+                for (int p = 0; p < kWX; ++p)
 #pragma unroll
-                for (int q = 0; q < DM; ++q)
+                    for (int q = 0; q < DM; ++q)
 #pragma unroll
-                    for (int k = 0; k < CPW; ++k)
+                        for (int k = 0; k < CPW; ++k)
 #pragma unroll
-                        for (int mt = 0; mt < 2; ++mt)
-                            Y[k][mt] = mfma(A[k][2 * DM + 2 + mt * DM + q][kWXa[p]],
-                                            XB[k][q][kWXx[p]], Y[k][mt]);
+                            for (int mt = 0; mt < 2; ++mt)
+                                Y[k][mt] = mfma(A[k][2 * DM + 2 + mt * DM + q][kWXa[p]],
+                                                XB[k][q][kWXx[p]], Y[k][mt]);
+            }
 #pragma unroll
             for (int k = 0; k < CPW; ++k)
 #pragma unroll
@@ -490,7 +529,7 @@ __global__ __launch_bounds__(kThreads) void mfma_prefill_kernel(
                         X[k][bg][q][i] = fmaf(l.x, xr, fmaf(-l.y, xi, Sr[k][q][i]));
                         X[k][bg][DM + q][i] = fmaf(l.x, xi, fmaf(l.y, xr, Si[k][q][i]));
                     }
-            stage_y(bg, Y);
+            if constexpr (MODE != kSegState) stage_y(bg, Y);
         }
     };
 
@@ -558,12 +597,14 @@ __global__ __launch_bounds__(kThreads) void mfma_prefill_kernel(
             const int r = tid + j * kThreads;
             const int rp = r % PPR, rt = (r / PPR) % kC, rb = r / (PPR * kC);
             const int64_t gt = t0 + rt;
-            if (r < NYP && b0 + rb < B && gt < T && c0 + rp * CPP < D) {
+            if (r < NYP && b0 + rb < BV && gt < TL && c0 + rp * CPP < D) {
                 uint4 v = *reinterpret_cast<const uint4*>(&ystage[rb * RS + rt * SD + 4 * rp]);
                 const int f = (rt >> 2) & 3;  // undo the word permutation of the piece
                 if (f & 1) v = make_uint4(v.y, v.x, v.w, v.z);
                 if (f & 2) v = make_uint4(v.z, v.w, v.x, v.y);
-                *reinterpret_cast<uint4*>(y + (int64_t(b0 + rb) * T + gt) * D + c0 + rp * CPP) = v;
+                const int rv = b0 + rb;
+                *reinterpret_cast<uint4*>(y + (int64_t(row_b(rv)) * T + int64_t(row_k(rv)) * TL + gt) * D +
+                                          c0 + rp * CPP) = v;
             }
         }
     };
@@ -575,7 +616,7 @@ __global__ __launch_bounds__(kThreads) void mfma_prefill_kernel(
     // outstanding accesses when the registers are consumed are the stores and
     // loads issued a whole compute phase before.  The last, partial chunk is
     // handled after the loop, so that the loop body holds no other path.
-    const int64_t nfull = T / kC;
+    const int64_t nfull = TL / kC;
     load_tile(0);
     store_tile(0);
     if (nch > 1) load_tile(1);
@@ -584,14 +625,16 @@ __global__ __launch_bounds__(kThreads) void mfma_prefill_kernel(
         compute_full();
         lds_barrier();  // tile consumed, stage complete
         if (kk + 1 < nch) store_tile(kk + 1);
-        write_y(kk);
+        if constexpr (MODE != kSegState) write_y(kk);
         if (kk + 2 < nch) load_tile(kk + 2);
         lds_barrier();  // next tile staged, stage free
     }
-    if (nch > nfull) {  // chunk nfull (staged)
-        compute_partial(int(T - nfull * kC));
-        lds_barrier();
-        write_y(nfull);
+    if constexpr (MODE == kWhole) {
+        if (nch > nfull) {  // chunk nfull (staged); segmented launches have none
+            compute_partial(int(T - nfull * kC));
+            lds_barrier();
+            write_y(nfull);
+        }
     }
 
     // ---- x_T
@@ -600,9 +643,12 @@ __global__ __launch_bounds__(kThreads) void mfma_prefill_kernel(
         const int c = c0 + w * CPW + k;
 #pragma unroll
         for (int bg = 0; bg < NBG; ++bg) {
-            const int b = b0 + kN * bg + n;
-            if (b < B && c < D) {
-                float2* dst = state + (int64_t(b) * D + c) * d;
+            const int r = b0 + kN * bg + n;
+            if (r < BV && c < D && (MODE != kSegOut || row_k(r) == SV - 1)) {
+                // x_T, or the end state s_k of segment k (from zero) in its slot
+                float2* dst = MODE == kSegState
+                                  ? xs + ((int64_t(row_b(r)) * nseg + row_k(r)) * D + c) * d
+                                  : state + (int64_t(row_b(r)) * D + c) * d;
 #pragma unroll
                 for (int q = 0; q < DM; ++q)
 #pragma unroll
@@ -620,21 +666,50 @@ int mfma_nbg(int64_t B, int64_t d, bool bf16_io)
     return d == 16 && !bf16_io && B > kN ? 2 : 1;
 }
 
-template <typename IO, int DM, int NBG>
+template <typename IO, int DM, int NBG, int MODE>
 hipError_t launch_main(const float2* lam, const void* u, void* y, float2* state,
                        const bf16x8* frag, const float2* lamc, int64_t B, int64_t D, int64_t T,
-                       hipStream_t stream)
+                       int nseg, int64_t seg_len, float2* xs, hipStream_t stream)
 {
     constexpr int CW = kW * Tiling<IO, DM>::CPW;
+    const int64_t sv = MODE == kWhole ? 1 : MODE == kSegState ? nseg - 1 : nseg;
     const int64_t ncg = (D + CW - 1) / CW;
-    const int64_t nbg = (B + kN * NBG - 1) / (kN * NBG);
+    const int64_t nbg = (B * sv + kN * NBG - 1) / (kN * NBG);
     const int64_t per_xcd = (ncg * nbg + 7) / 8;  // logical workgroups per XCD
     const int64_t grid = 8 * per_xcd;
-    if (grid > 0x7fffffff) return hipErrorInvalidConfiguration;
-    hipLaunchKernelGGL((mfma_prefill_kernel<IO, DM, NBG>), dim3(uint32_t(grid)), dim3(kThreads),
-                       0, stream, lam, static_cast<const IO*>(u), static_cast<IO*>(y), state,
-                       frag, lamc, int(B), int(D), T, int(ncg), int(nbg), int(per_xcd));
+    if (grid > 0x7fffffff || B * sv > 0x7fffffff) return hipErrorInvalidConfiguration;
+    hipLaunchKernelGGL((mfma_prefill_kernel<IO, DM, NBG, MODE>), dim3(uint32_t(grid)),
+                       dim3(kThreads), 0, stream, lam, static_cast<const IO*>(u),
+                       static_cast<IO*>(y), state, frag, lamc, int(B), int(D), T, int(ncg),
+                       int(nbg), int(per_xcd), nseg, seg_len, xs);
     return hipGetLastError();
+}
+
+template <int MODE>
+hipError_t launch_mode(const float2* lam, const void* u, bool bf16_io, int64_t B, int64_t D,
+                       int64_t d, int64_t T, float2* state, void* y, const void* workspace,
+                       int nseg, int64_t seg_len, float2* xs, hipStream_t stream)
+{
+    const int DM = int(d / 16);
+    const size_t frag_bytes = size_t(D) * n_frag(DM) * kTerms * 64 * sizeof(bf16x8);
+    const bf16x8* frag = static_cast<const bf16x8*>(workspace);
+    const float2* lamc = reinterpret_cast<const float2*>(static_cast<const char*>(workspace) +
+                                                         (frag_bytes + 255) / 256 * 256);
+    // rows of the MFMA columns: batch rows or (batch row, segment) pairs
+    const int64_t rows = MODE == kWhole ? B : MODE == kSegState ? B * (nseg - 1) : B * nseg;
+    const bool two = mfma_nbg(rows, d, bf16_io) == 2;
+    if (bf16_io)
+        return DM == 2 ? launch_main<bf16, 2, 1, MODE>(lam, u, y, state, frag, lamc, B, D, T,
+                                                       nseg, seg_len, xs, stream)
+                       : launch_main<bf16, 1, 1, MODE>(lam, u, y, state, frag, lamc, B, D, T,
+                                                       nseg, seg_len, xs, stream);
+    if (DM == 2)
+        return launch_main<float, 2, 1, MODE>(lam, u, y, state, frag, lamc, B, D, T, nseg,
+                                              seg_len, xs, stream);
+    return two ? launch_main<float, 1, 2, MODE>(lam, u, y, state, frag, lamc, B, D, T, nseg,
+                                                seg_len, xs, stream)
+               : launch_main<float, 1, 1, MODE>(lam, u, y, state, frag, lamc, B, D, T, nseg,
+                                                seg_len, xs, stream);
 }
 
 }  // namespace
@@ -654,6 +729,21 @@ bool mfma_supported(int64_t B, int64_t D, int64_t d, int64_t T)
            D <= (INT64_C(1) << 30);
 }
 
+// Segmented plan: the fewest segments (a power of two, each a multiple of 32
+// and at least 256 steps long) whose (batch row, segment) columns give at
+// least kSegWorkgroups workgroups of 8 channels, else the most segments
+// allowed.
+int64_t mfma_segments(int64_t B, int64_t D, int64_t T)
+{
+    constexpr int64_t kSegWorkgroups = 1024, kMinSeg = 256;
+    int64_t best = 0;
+    for (int64_t s = 2; T % (s * kC) == 0 && T / s >= kMinSeg; s *= 2) {
+        best = s;
+        if ((B * s + kN - 1) / kN * ((D + kW - 1) / kW) >= kSegWorkgroups) break;
+    }
+    return best;
+}
+
 // The matrix-core plan has no parallelism along time: the automatic plan takes
 // it when its workgroups alone fill the GPU, counted as 16 channels x 32 batch
 // rows (two rounds of the bfloat16 tiling with d = 16, 16 x 16).  The choice must not depend on the
@@ -664,10 +754,8 @@ bool mfma_preferred(int64_t B, int64_t D, int64_t d)
     return ((D + 15) / 16) * ((B + 31) / 32) >= kMinWorkgroups;
 }
 
-hipError_t launch_prefill_mfma(const float2* lam, const float2* R, const float* h0,
-                               const void* u, bool bf16_io, int64_t B, int64_t D, int64_t d,
-                               int64_t T, float2* state, void* y, void* workspace,
-                               hipStream_t stream)
+hipError_t launch_mfma_setup(const float2* lam, const float2* R, const float* h0, int64_t D,
+                             int64_t d, void* workspace, hipStream_t stream)
 {
     (void)hipGetLastError();
     const int DM = int(d / 16);
@@ -682,15 +770,32 @@ hipError_t launch_prefill_mfma(const float2* lam, const float2* R, const float* 
     else
         hipLaunchKernelGGL(mfma_setup_kernel<2>, dim3(uint32_t(D)), dim3(256), 0, stream, lam,
                            R, h0, frag, lamc);
-    hipError_t e = hipGetLastError();
+    return hipGetLastError();
+}
+
+hipError_t launch_prefill_mfma(const float2* lam, const float2* R, const float* h0,
+                               const void* u, bool bf16_io, int64_t B, int64_t D, int64_t d,
+                               int64_t T, float2* state, void* y, void* workspace,
+                               hipStream_t stream)
+{
+    hipError_t e = launch_mfma_setup(lam, R, h0, D, d, workspace, stream);
     if (e != hipSuccess) return e;
-    const bool two = mfma_nbg(B, d, bf16_io) == 2;
-    if (bf16_io)
-        return DM == 2 ? launch_main<bf16, 2, 1>(lam, u, y, state, frag, lamc, B, D, T, stream)
-                       : launch_main<bf16, 1, 1>(lam, u, y, state, frag, lamc, B, D, T, stream);
-    if (DM == 2) return launch_main<float, 2, 1>(lam, u, y, state, frag, lamc, B, D, T, stream);
-    return two ? launch_main<float, 1, 2>(lam, u, y, state, frag, lamc, B, D, T, stream)
-               : launch_main<float, 1, 1>(lam, u, y, state, frag, lamc, B, D, T, stream);
+    return launch_mode<kWhole>(lam, u, bf16_io, B, D, d, T, state, y, workspace, 1, T, nullptr,
+                               stream);
+}
+
+hipError_t launch_mfma_segment_pass(bool outputs, const float2* lam, const void* u,
+                                    bool bf16_io, int64_t B, int64_t D, int64_t d, int64_t T,
+                                    int nseg, int64_t seg_len, float2* xs, float2* state,
+                                    void* y, const void* workspace, hipStream_t stream)
+{
+    (void)hipGetLastError();
+    if (seg_len % kC != 0 || int64_t(nseg) * seg_len != T || nseg < 2)
+        return hipErrorInvalidValue;
+    return outputs ? launch_mode<kSegOut>(lam, u, bf16_io, B, D, d, T, state, y, workspace, nseg,
+                                          seg_len, xs, stream)
+                   : launch_mode<kSegState>(lam, u, bf16_io, B, D, d, T, state, y, workspace,
+                                            nseg, seg_len, xs, stream);
 }
 
 }  // namespace lh

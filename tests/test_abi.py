@@ -81,9 +81,17 @@ def test_workspace_sizes():
     assert lh.workspace_bytes(64, 2048, 16, 4096) == -(-frag(2048, 16) // 256) * 256 + 2048 * 16 * 8
     # the explicit matrix-core plan needs the same tables
     assert lh.workspace_bytes(4, 1024, 32, 65536, chunk_len=-1) == frag(1024, 32) + 1024 * 32 * 8
-    # long prompt, few rows: the automatic plan keeps the VALU chunked scan
-    # (32 chunks of 2048 steps) for its parallelism along time
-    assert lh.workspace_bytes(4, 1024, 32, 65536) == 1024 * 32 * 8 + 4 * 32 * 1024 * 32 * 8
+    # long prompt, few rows: the automatic plan cuts the prompt into 32 segments
+    # of 2048 steps on the matrix cores (lambda^C, segment entry states, then
+    # the matrix-core tables)
+    up = lambda x: -(-x // 256) * 256  # noqa: E731
+    seg_ws = up(1024 * 32 * 8) + up(4 * 32 * 1024 * 32 * 8) + frag(1024, 32) + 1024 * 32 * 8
+    assert lh.workspace_bytes(4, 1024, 32, 65536) == seg_ws
+    assert lh.workspace_bytes(4, 1024, 32, 65536, chunk_len=-2) == seg_ws
+    # the VALU chunked scan when asked for (32 chunks of 2048 steps)
+    assert lh.workspace_bytes(4, 1024, 32, 65536, chunk_len=2048) == 1024 * 32 * 8 + 4 * 32 * 1024 * 32 * 8
+    # the segmented plan needs segments of >= 256 steps, a multiple of 32
+    assert lh.lib().lh_prefill_workspace_bytes(4, 1024, 32, 500, -2) == ctypes.c_size_t(-1).value
     # the matrix-core plan needs d = 16 / 32 and D % 8 == 0
     bad = ctypes.c_size_t(-1).value
     assert lh.lib().lh_prefill_workspace_bytes(2, 12, 16, 64, -1) == bad
@@ -95,7 +103,8 @@ def test_workspace_sizes():
     L = lh.lib()
     bad = ctypes.c_size_t(-1).value
     for args in [(0, 1, 1, 1, 0), (1, 0, 1, 1, 0), (1, 1, 0, 1, 0), (1, 1, 1025, 1, 0),
-                 (1, 1, 1, -1, 0), (1, 1, 1, 1, -1), (1 << 40, 1 << 20, 64, 1 << 20, 0)]:
+                 (1, 1, 1, -1, 0), (1, 1, 1, 1, -1), (1, 1, 1, 1, -3),
+                 (1 << 40, 1 << 20, 64, 1 << 20, 0)]:
         assert L.lh_prefill_workspace_bytes(*args) == bad, args
 
 
@@ -123,7 +132,8 @@ def step_args(**kw):
     (dict(lam=None), 1), (dict(R=None), 1), (dict(h0=None), 1), (dict(state=None), 1),
     (dict(u=None), 1), (dict(y=None), 1),
     (dict(B=0), 1), (dict(D=-3), 1), (dict(d=0), 1), (dict(d=1025), 1), (dict(T=-1), 1),
-    (dict(chunk=-2), 1),
+    (dict(chunk=-3), 1),
+    (dict(chunk=-2), 1),                 # segmented plan: d = 4 unsupported
     (dict(B=1 << 40, D=1 << 20), 1),  # element count overflow
     (dict(io=7), 3),
     (dict(u=A + 3 * MB + 2), 1),  # misaligned float32 input

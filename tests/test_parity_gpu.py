@@ -82,6 +82,13 @@ SMALL = [
     (40, 16, 16, 200, 3, "f32", -1),   # 2 batch groups per workgroup (float32), ragged
     (20, 8, 16, 65, 2, "bf16", -1),    # 2 batch groups per workgroup (bfloat16)
     (5, 67, 2, 33, 6, "bf16", 0),      # d = 2: one lane per row, B not a multiple of 4
+    # segmented matrix-core prefill (chunk_len = -2 = LH_PREFILL_MFMA_SEG: T cut into
+    # 2^k segments of >= 256 steps; each (batch row, segment) pair is a matrix column)
+    (2, 64, 16, 512, 5, "f32", -2),    # two segments of 256 steps
+    (3, 136, 16, 1024, 5, "bf16", -2), # four segments, 17 channel groups, bfloat16
+    (1, 16, 32, 2048, 4, "f32", -2),   # d = 32, eight segments
+    (5, 40, 32, 4096, 3, "bf16", -2),  # d = 32, bfloat16, 16 segments, 5 rows
+    (40, 16, 16, 1024, 3, "f32", -2),  # 2 column groups per wave (float32, d = 16)
 ]
 
 
