@@ -242,6 +242,15 @@ struct Stage<float> {
 // Segmented launches need seg_len % C == 0 and T == nseg seg_len.
 enum { kWhole = 0, kSegState = 1, kSegOut = 2 };
 
+// Channels per wave: the state-only pass holds only the P operands (a third
+// of the A registers), so its waves take more channels and read wider pieces
+// of each line of u.
+template <typename IO, int DM, int MODE>
+constexpr int cpw_of()
+{
+    return MODE == kSegState ? (sizeof(IO) == 2 && DM == 1 ? 4 : 2) : Tiling<IO, DM>::CPW;
+}
+
 template <typename IO, int DM, int NBG, int MODE>
 __global__ __launch_bounds__(kThreads) void mfma_prefill_kernel(
     const float2* __restrict__ lam, const IO* __restrict__ u, IO* __restrict__ y,
@@ -251,7 +260,7 @@ __global__ __launch_bounds__(kThreads) void mfma_prefill_kernel(
 {
     constexpr int d = 16 * DM;
     constexpr int F = n_frag(DM);
-    constexpr int CPW = Tiling<IO, DM>::CPW;
+    constexpr int CPW = cpw_of<IO, DM, MODE>();
     constexpr int CW = kW * CPW;
     constexpr int BN = kN * NBG;                      // batch rows per workgroup
     constexpr int NTU = Stage<IO>::kNTU;
@@ -271,7 +280,7 @@ __global__ __launch_bounds__(kThreads) void mfma_prefill_kernel(
     constexpr int RS = kC * SD + 4;                   // words per row
     constexpr int NYP = BN * kC * PPR;                // 16-byte output pieces per chunk
     __shared__ __attribute__((aligned(16))) ST ubuf[CW * BN * US];
-    __shared__ __attribute__((aligned(16))) uint32_t ystage[BN * RS];
+    __shared__ __attribute__((aligned(16))) uint32_t ystage[MODE == kSegState ? 1 : BN * RS];
     __shared__ __attribute__((aligned(16))) float2 lcs[CW][4][4 * DM];  // lambda^C per channel, lane group
 
     // ---- workgroup -> (channel group, batch group); logical index lin runs
@@ -671,7 +680,7 @@ hipError_t launch_main(const float2* lam, const void* u, void* y, float2* state,
                        const bf16x8* frag, const float2* lamc, int64_t B, int64_t D, int64_t T,
                        int nseg, int64_t seg_len, float2* xs, hipStream_t stream)
 {
-    constexpr int CW = kW * Tiling<IO, DM>::CPW;
+    constexpr int CW = kW * cpw_of<IO, DM, MODE>();
     const int64_t sv = MODE == kWhole ? 1 : MODE == kSegState ? nseg - 1 : nseg;
     const int64_t ncg = (D + CW - 1) / CW;
     const int64_t nbg = (B * sv + kN * NBG - 1) / (kN * NBG);
