@@ -293,3 +293,31 @@ def test_bf16_outputs_round_half_to_even():
     # the ties really are ties: the float32 product is not a bfloat16 value
     prod = u.float() * h0.cpu()
     assert bool((prod.to(torch.bfloat16).float() != prod).float().mean() > 0.9)
+
+
+@pytest.mark.parametrize("io", ["f32", "bf16"])
+def test_unaligned_io_falls_back_to_the_vector_scan(io):
+    """u and y one element past a 16-byte boundary: the automatic matrix-core
+    plans (whole prompt, and segmented) run the VALU chunked scan instead,
+    with the same workspace, and still match the oracle."""
+    import torch
+
+    import paper_2310_18780_amd as lh
+
+    for B, D, d, T in ((2, 64, 16, 1024), (32, 4096, 16, 8)):  # segmented / whole-prompt plans
+        w, (lam, R, h0, up, ud) = small_case(B, D, d, T, 0, io)
+        ref = oracle.run(lam, R, h0, up, ud)
+        t = to_device(lam, R, h0, up, ud, io)
+        n = B * T * D
+        ubuf = torch.empty(n + 1, dtype=t["u"].dtype, device="cuda")
+        ybuf = torch.full((n + 1,), float("nan"), dtype=t["u"].dtype, device="cuda")
+        u = ubuf[1:].view(B, T, D)
+        u.copy_(t["u"])
+        y = ybuf[1:].view(B, T, D)
+        assert u.data_ptr() % 16 != 0 and y.data_ptr() % 16 != 0
+        state = torch.empty((B, D, d), dtype=torch.complex64, device="cuda")
+        lh.prefill(t["lam"], t["R"], t["h0"], u, state, y)
+        torch.cuda.synchronize()
+        yp = _np(y).transpose(0, 2, 1).reshape(B * D, T)
+        check_y(yp, ref["y_prefill"].transpose(0, 2, 1).reshape(B * D, T), io, "unaligned prefill y")
+        check_x(_np(state).reshape(-1, d), ref["x_T"].reshape(-1, d), "unaligned prefill x_T")
