@@ -619,7 +619,7 @@ def companion_main(args):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py: this build runs on exactly one GPU; --gpus {args.gpus} is not "
+        print(f"bench.py: this benchmark runs on exactly one GPU; --gpus {args.gpus} is not "
               f"supported (every (b, c) row is independent, so batch/channel sharding needs "
               f"no exchange; it is not built here).", file=sys.stderr)
         sys.exit(2)
@@ -765,7 +765,7 @@ def main():
         "decode_gbps": dec_gbs,
         "roofline": {"bound": "hbm", "achieved": dec_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": dec_gbs / HBM_PEAK_GBS, "traffic": traffic,
-                     "kernel": "step_kernel", "bytes_per_launch": dbytes},
+                     "kernel": "step_pairs_kernel", "bytes_per_launch": dbytes},
         "roofline_prefill": {"bound": "alu", "achieved": pre_tf, "peak": FP32_VALU_PEAK_TFLOPS,
                              "unit": "TFLOP/s", "frac": pre_tf / FP32_VALU_PEAK_TFLOPS,
                              "traffic": traffic_pre, "flops_per_launch": prefill_flops(w),
