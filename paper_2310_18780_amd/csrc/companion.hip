@@ -91,9 +91,37 @@ __global__ __launch_bounds__(64) void companion_coeffs_kernel(const float2* __re
 
 // G = 2^k >= d lanes per (b, c) row, lane j holding the state pair
 // (x[2j], x[2j+1]) (16 bytes: a wave moves contiguous kilobytes).  The two
-// dot products are reduced over the row's lanes with butterfly shuffles; the
-// shift takes x[2j-1] from the lane below.
+// dot products are reduced over the row's lanes with DPP row permutations;
+// the shift takes x[2j-1] from the lane below (DPP row shift).  Each thread serves kRows batch
+// rows of one channel, so the channel's coefficient pair is loaded once for
+// them; the grid is (channel tile, batch group).
 constexpr int next_pow2(int x) { return x <= 1 ? 1 : 2 * next_pow2((x + 1) / 2); }
+constexpr int kRows = 4;
+
+// A float64 moved across lanes by a DPP row permutation (both 32-bit halves).
+template <int CTRL>
+__device__ __forceinline__ double dpp_move(double v)
+{
+    const unsigned long long bits = __builtin_bit_cast(unsigned long long, v);
+    const int lo = __builtin_amdgcn_mov_dpp(static_cast<int>(bits & 0xffffffffu), CTRL, 0xF, 0xF,
+                                            false);
+    const int hi = __builtin_amdgcn_mov_dpp(static_cast<int>(bits >> 32), CTRL, 0xF, 0xF, false);
+    return __builtin_bit_cast(double, static_cast<unsigned long long>(static_cast<unsigned>(lo)) |
+                                         (static_cast<unsigned long long>(static_cast<unsigned>(hi))
+                                          << 32));
+}
+
+// Sum over the G (a power of two <= 16) lanes of an aligned group: quad
+// permutations, then the half-row and row mirrors; every lane gets the sum.
+template <int G>
+__device__ __forceinline__ double group_sum(double v)
+{
+    if constexpr (G >= 2) v += dpp_move<0xB1>(v);   // quad_perm [1,0,3,2]
+    if constexpr (G >= 4) v += dpp_move<0x4E>(v);   // quad_perm [2,3,0,1]
+    if constexpr (G >= 8) v += dpp_move<0x141>(v);  // row_half_mirror
+    if constexpr (G >= 16) v += dpp_move<0x140>(v); // row_mirror
+    return v;
+}
 
 template <typename IO, int ORD>
 __global__ __launch_bounds__(kThreads) void companion_step_kernel(
@@ -103,32 +131,44 @@ __global__ __launch_bounds__(kThreads) void companion_step_kernel(
 {
     constexpr int P = ORD / 2;           // state pairs per row
     constexpr int G = next_pow2(P);      // lanes per row
-    const int64_t gid = int64_t(blockIdx.x) * kThreads + threadIdx.x;
-    const int64_t row = gid / G;         // b * D + c
-    const int j = static_cast<int>(gid % G);
-    const bool live = row < B * D;       // whole groups leave together: no exits before shuffles
-    const int64_t rr = live ? row : 0;
-    const int64_t c = rr % D;
-    const bool own = live && j < P;
-    double2 x = make_double2(0.0, 0.0), av = x, bv = x;
+    const int64_t c = int64_t(blockIdx.x) * (kThreads / G) + threadIdx.x / G;
+    const int j = threadIdx.x % G;
+    const int64_t b0 = int64_t(blockIdx.y) * kRows;
+    // lanes past D or past the pairs compute on zeros and store nothing; no
+    // exits before the shuffles
+    const bool own = c < D && j < P;
+    const int64_t cc = c < D ? c : D - 1;
+    double2 av = make_double2(0.0, 0.0), bv = av;
     if (own) {
-        x = reinterpret_cast<const double2*>(state + rr * ORD)[j];
-        av = reinterpret_cast<const double2*>(a + c * ORD)[j];
-        bv = reinterpret_cast<const double2*>(beta + c * ORD)[j];
+        av = reinterpret_cast<const double2*>(a + cc * ORD)[j];
+        bv = reinterpret_cast<const double2*>(beta + cc * ORD)[j];
     }
-    double out = fma(bv.x, x.x, bv.y * x.y);
-    double fb = fma(av.x, x.x, av.y * x.y);
+    double2 x[kRows];
+    double ut[kRows];
 #pragma unroll
-    for (int m = 1; m < G; m *= 2) {
-        out += __shfl_xor(out, m, G);
-        fb += __shfl_xor(fb, m, G);
+    for (int i = 0; i < kRows; ++i) {
+        const int64_t b = b0 + i < B ? b0 + i : B - 1;
+        const int64_t row = b * D + cc;
+        x[i] = own ? reinterpret_cast<const double2*>(state + row * ORD)[j]
+                   : make_double2(0.0, 0.0);
+        ut[i] = io_load(u + row);
     }
-    const double below = __shfl_up(x.y, 1, G);  // x[2j-1]
-    if (!own) return;
-    const double ut = io_load(u + rr);
-    if (j == 0) io_store(y + rr, static_cast<float>(fma(static_cast<double>(h0[c]), ut, out)));
-    reinterpret_cast<double2*>(state + rr * ORD)[j] =
-        make_double2(j == 0 ? ut - fb : below, x.x);
+    const double hz = h0[cc];
+#pragma unroll
+    for (int i = 0; i < kRows; ++i) {
+        double out = fma(bv.x, x[i].x, bv.y * x[i].y);
+        double fb = fma(av.x, x[i].x, av.y * x[i].y);
+        out = group_sum<G>(out);
+        fb = group_sum<G>(fb);
+        const double below = dpp_move<0x111>(x[i].y);  // row_shr:1: x[2j-1] (unused at j = 0)
+        const int64_t b = b0 + i;
+        if (own && b < B) {
+            const int64_t row = b * D + c;
+            if (j == 0) io_store(y + row, static_cast<float>(fma(hz, ut[i], out)));
+            reinterpret_cast<double2*>(state + row * ORD)[j] =
+                make_double2(j == 0 ? ut[i] - fb : below, x[i].x);
+        }
+    }
 }
 
 // g_t for t < T per channel (one thread per channel): g_0 = 1,
@@ -244,14 +284,16 @@ template <typename IO>
 hipError_t step_io(const double* a, const double* beta, const float* h0, double* state,
                    const void* u_t, void* y_t, int64_t B, int64_t D, int64_t d, hipStream_t s)
 {
-    uint32_t g;
-    if (!blocks(B * D * next_pow2(static_cast<int>(d)), &g)) return hipErrorInvalidConfiguration;
+    const int64_t per_block = kThreads / next_pow2(static_cast<int>(d));  // channels per block
+    const int64_t gx = (D + per_block - 1) / per_block, gy = (B + kRows - 1) / kRows;
+    if (gx > 0x7fffffff || gy > 0xffff) return hipErrorInvalidConfiguration;
+    const dim3 g(static_cast<uint32_t>(gx), static_cast<uint32_t>(gy));
     switch (2 * d) {
 #define LH_CASE(O)                                                                              \
     case O:                                                                                     \
-        hipLaunchKernelGGL((companion_step_kernel<IO, O>), dim3(g), dim3(kThreads), 0, s, a,    \
-                           beta, h0, state, static_cast<const IO*>(u_t), static_cast<IO*>(y_t), \
-                           B, D);                                                               \
+        hipLaunchKernelGGL((companion_step_kernel<IO, O>), g, dim3(kThreads), 0, s, a, beta,    \
+                           h0, state, static_cast<const IO*>(u_t), static_cast<IO*>(y_t), B,    \
+                           D);                                                                  \
         break;
         LH_COMPANION_ORDERS(LH_CASE)
 #undef LH_CASE
