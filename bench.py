@@ -58,6 +58,10 @@ def parse():
                    help="time the companion-form decode step and fast initialisation beside the "
                         "modal ones on --companion-workload")
     p.add_argument("--companion-workload", default="cp")
+    p.add_argument("--launch-floor", action="store_true",
+                   help="time plain kernels with the decode step's footprint on --workload "
+                        "(an empty launch, an in-place update and a copy of the state's bytes), "
+                        "graph-replayed like the decode steps")
     p.add_argument("--distill", action="store_true",
                    help="time the distillation objective (lh_distill) on --workload's filter "
                         "bank with L = its T")
@@ -616,6 +620,50 @@ def companion_main(args):
     print(json.dumps(out), flush=True)
 
 
+def launch_floor_main(args):
+    """Reference points for the decode step: per-launch times of plain torch
+    kernels with the step's footprint (the state's bytes), replayed K at a time
+    from a graph exactly as the decode steps are."""
+    import torch
+
+    import workloads
+
+    w = workloads.workload(args.workload)
+    nbytes = 8 * w.B * w.D * w.d
+    a = torch.zeros(nbytes // 4, device="cuda")
+    b = torch.zeros_like(a)
+    K = w.K
+
+    def per_launch_us(fn):
+        fn()
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for _ in range(K):
+                fn()
+        g.replay()
+        torch.cuda.synchronize()
+        s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        t = []
+        for _ in range(max(3, args.steps // 4)):
+            s.record()
+            g.replay()
+            e.record()
+            torch.cuda.synchronize()
+            t.append(s.elapsed_time(e) * 1e3 / K)
+        return sorted(t)[len(t) // 2]
+
+    out = {
+        "metric": "per-launch time of reference kernels with the decode step's footprint",
+        "config": {"workload": w.name, "state_bytes": nbytes, "launches_per_graph": K},
+        "empty_launch_us": per_launch_us(lambda: a[:1].add_(1.0)),
+        "inplace_add_state_bytes_us": per_launch_us(lambda: a.add_(1.0)),
+        "copy_state_bytes_us": per_launch_us(lambda: b.copy_(a)),
+        "decode_step_bytes": decode_bytes(w),
+    }
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -637,6 +685,9 @@ def main():
         return
     if args.companion:
         companion_main(args)
+        return
+    if args.launch_floor:
+        launch_floor_main(args)
         return
 
     import torch
