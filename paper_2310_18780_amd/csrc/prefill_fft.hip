@@ -695,7 +695,7 @@ hipError_t run(const float2* lam, const float2* R, const float* h0, const IO* u,
     const int nmc = static_cast<int>((d + kSM - 1) / kSM);
     const int nmcg = (nmc + kThreads / 64 - 1) / (kThreads / 64);
     const int64_t nrg = (B + kSR - 1) / kSR;
-    if (nrg * nmcg > 0x7fffffff || p.nparts > 0xffff) return hipErrorInvalidConfiguration;
+    if (nrg * nmcg > 0xffff || p.nparts > 0xffff) return hipErrorInvalidConfiguration;
     float2* out = p.nparts > 1 ? reinterpret_cast<float2*>(ws + p.off_parts) : state;
     hipLaunchKernelGGL((fft_state_kernel<IO>),
                        dim3(gc, static_cast<uint32_t>(p.nparts), static_cast<uint32_t>(nrg * nmcg)),
@@ -719,6 +719,8 @@ bool make_fft_plan(int64_t B, int64_t D, int64_t d, int64_t T, FftPlan* plan)
     FftPlan p{};
     p.npair = (B + 1) / 2;
     if (p.npair > 0xffff) return false;  // grid z of the transform passes
+    // grid z of the state contraction: batch groups x mode-chunk groups
+    if ((B + kSR - 1) / kSR * ((d + 4 * kSM - 1) / (4 * kSM)) > 0xffff) return false;
     if (T == 0) {
         *plan = p;
         return true;
