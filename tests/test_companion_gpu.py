@@ -103,6 +103,7 @@ STEP_CASES = [
     (2, 300, 4, 0, 7, "f32", (0.5, 0.95)),   # from the zero state
     (1, 5, 3, 2, 4, "bf16", (0.5, 0.9)),     # prompt shorter than the order
     (4, 257, 2, 1000, 3, "f32", (0.9, 0.999)),
+    (5, 1, 4, 80, 4, "bf16", (0.5, 0.95)),   # a single channel
 ]
 
 

@@ -82,6 +82,8 @@ SMALL = [
     (40, 16, 16, 200, 3, "f32", -1),   # 2 batch groups per workgroup (float32), ragged
     (20, 8, 16, 65, 2, "bf16", -1),    # 2 batch groups per workgroup (bfloat16)
     (5, 67, 2, 33, 6, "bf16", 0),      # d = 2: one lane per row, B not a multiple of 4
+    (3, 1, 16, 90, 5, "f32", 0),       # a single channel
+    (2, 1, 5, 70, 4, "bf16", 16),      # a single channel, chunked, generic decode
     # segmented matrix-core prefill (chunk_len = -2 = LH_PREFILL_MFMA_SEG: T cut into
     # 2^k segments of >= 256 steps; each (batch row, segment) pair is a matrix column)
     (2, 64, 16, 512, 5, "f32", -2),    # two segments of 256 steps

@@ -82,6 +82,7 @@ SMALL = [
     (4, 64, 32, 4096, 3, "f32"),   # N = 8192 (128 x 64)
     (2, 40, 16, 2049, 3, "bf16"),  # T just past a power of two: N = 8192
     (6, 24, 8, 513, 2, "f32"),     # three pairs
+    (3, 1, 16, 700, 2, "f32"),     # a single channel
 ]
 
 
