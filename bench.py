@@ -818,10 +818,15 @@ def main():
         "decode_gbps": dec_gbs,
         "roofline": {"bound": "hbm", "achieved": dec_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": dec_gbs / HBM_PEAK_GBS, "traffic": traffic,
+                     "traffic_gbps": (traffic / (dec_launch_us * 1e-6) / 1e9
+                                      if traffic is not None else None),
                      "kernel": "step_pairs_kernel", "bytes_per_launch": dbytes},
         "roofline_prefill": {"bound": "alu", "achieved": pre_tf, "peak": FP32_VALU_PEAK_TFLOPS,
                              "unit": "TFLOP/s", "frac": pre_tf / FP32_VALU_PEAK_TFLOPS,
-                             "traffic": traffic_pre, "flops_per_launch": prefill_flops(w),
+                             "traffic": traffic_pre,
+                             "traffic_gbps": (traffic_pre / (pre_avg * 1e-3) / 1e9
+                                              if traffic_pre is not None else None),
+                             "flops_per_launch": prefill_flops(w),
                              "bytes_per_launch": prefill_bytes(w),
                              "gbps": prefill_bytes(w) / (pre_avg * 1e-3) / 1e9,
                              "mfma_busy": profile_value(f"prefill_{w.name}_sq_counters.txt",
