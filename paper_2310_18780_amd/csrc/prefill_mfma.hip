@@ -58,7 +58,9 @@ namespace lh {
 namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
 
 constexpr int kC = 32;     // chunk length = K of the MFMA
 constexpr int kN = 16;     // batch rows per MFMA column block
@@ -75,6 +77,25 @@ __device__ __forceinline__ void split3(float v, __bf16& a, __bf16& b, __bf16& c)
     b = static_cast<__bf16>(r1);
     const float r2 = r1 - static_cast<float>(b);
     c = static_cast<__bf16>(r2);
+}
+
+// nearest bfloat16 values of a pair (one packed conversion), and the
+// bfloat16 residuals of the pair after them
+__device__ __forceinline__ bf16x2 to_bf16x2(float a, float b)
+{
+    return __builtin_convertvector(f32x2{a, b}, bf16x2);
+}
+
+__device__ __forceinline__ bf16x2 residual_bf16x2(float a, float b, bf16x2 h)
+{
+    const f32x2 back = __builtin_convertvector(h, f32x2);
+    return to_bf16x2(a - back.x, b - back.y);
+}
+
+__device__ __forceinline__ bf16x8 concat4(bf16x2 a, bf16x2 b, bf16x2 c, bf16x2 d)
+{
+    return __builtin_shufflevector(__builtin_shufflevector(a, b, 0, 1, 2, 3),
+                                   __builtin_shufflevector(c, d, 0, 1, 2, 3), 0, 1, 2, 3, 4, 5, 6, 7);
 }
 
 __device__ __forceinline__ f32x4 mfma(bf16x8 a, bf16x8 b, f32x4 c)
@@ -251,6 +272,18 @@ constexpr int cpw_of()
     return MODE == kSegState ? (sizeof(IO) == 2 && DM == 1 ? 4 : 2) : Tiling<IO, DM>::CPW;
 }
 
+// Chunk tiles of u in flight while a chunk is computed (in registers, one
+// per tile): two where the registers allow it without spilling inside the
+// chunk loop (bfloat16 inputs with d = 16).  The waves of a workgroup run in
+// step through its barriers and there are only two per SIMD, so with one tile
+// in flight each chunk waits out a whole memory latency; a second tile hides
+// most of it.
+template <typename IO, int DM, int MODE>
+constexpr int pf_of()
+{
+    return sizeof(IO) == 2 && DM == 1 && MODE != kSegState ? 2 : 1;
+}
+
 template <typename IO, int DM, int NBG, int MODE>
 __global__ __launch_bounds__(kThreads) void mfma_prefill_kernel(
     const float2* __restrict__ lam, const IO* __restrict__ u, IO* __restrict__ y,
@@ -367,8 +400,9 @@ __global__ __launch_bounds__(kThreads) void mfma_prefill_kernel(
         src0[j] = u + (int64_t(row_b(r)) * T + int64_t(row_k(r)) * TL + 2 * itp) * D +
                   min(c0 + ip * CPP, D - CPP);
     }
-    uint4 R0[IPT][2];
-    auto load_tile = [&](int64_t kk) {
+    constexpr int PF = pf_of<IO, DM, MODE>();
+    uint4 RA[IPT][2], RB[PF == 2 ? IPT : 1][2];
+    auto load_tile = [&](int64_t kk, auto& R0) {
         if ((kk + 1) * kC <= TL) {  // full chunk (uniform branch)
             const int64_t off = kk * kC * D;
 #pragma unroll
@@ -390,7 +424,7 @@ __global__ __launch_bounds__(kThreads) void mfma_prefill_kernel(
             }
         }
     };
-    auto store_tile = [&](int64_t kk) {
+    auto store_tile = [&](int64_t kk, const auto& R0) {
 #pragma unroll
         for (int j = 0; j < IPT; ++j) {
             if (tid + j * kThreads >= NITEM) continue;
@@ -399,18 +433,19 @@ __global__ __launch_bounds__(kThreads) void mfma_prefill_kernel(
             const bool in = b0 + irb < BV && c0 + ip * CPP < D;
             const bool ok0 = in && kk * kC + 2 * itp < TL;
             const bool ok1 = in && kk * kC + 2 * itp + 1 < TL;
+            const uint4 z = make_uint4(0u, 0u, 0u, 0u);
+            const uint4 s0 = ok0 ? R0[j][0] : z, s1 = ok1 ? R0[j][1] : z;
 #pragma unroll
             for (int ch = 0; ch < CPP; ++ch) {
                 const int e = ((ip * CPP + ch) * BN + irb) * US + 2 * itp;  // element of step 2 itp
-                if constexpr (ES == 2) {
-                    const uint32_t w0 = ok0 ? reinterpret_cast<const uint32_t*>(&R0[j][0])[ch / 2] : 0u;
-                    const uint32_t w1 = ok1 ? reinterpret_cast<const uint32_t*>(&R0[j][1])[ch / 2] : 0u;
-                    const uint32_t lo = ch % 2 == 0 ? (w0 & 0xffffu) : (w0 >> 16);
-                    const uint32_t hi = ch % 2 == 0 ? (w1 & 0xffffu) : (w1 >> 16);
-                    reinterpret_cast<uint32_t*>(ubuf)[e / 2] = lo | (hi << 16);
+                if constexpr (ES == 2) {  // (step 2 itp, step 2 itp + 1) of channel ch
+                    const uint32_t w0 = reinterpret_cast<const uint32_t*>(&s0)[ch / 2];
+                    const uint32_t w1 = reinterpret_cast<const uint32_t*>(&s1)[ch / 2];
+                    reinterpret_cast<uint32_t*>(ubuf)[e / 2] =
+                        ch % 2 == 0 ? (w0 & 0xffffu) | (w1 << 16) : (w0 >> 16) | (w1 & 0xffff0000u);
                 } else {
-                    const float v0 = ok0 ? reinterpret_cast<const float*>(&R0[j][0])[ch] : 0.f;
-                    const float v1 = ok1 ? reinterpret_cast<const float*>(&R0[j][1])[ch] : 0.f;
+                    const float v0 = reinterpret_cast<const float*>(&s0)[ch];
+                    const float v1 = reinterpret_cast<const float*>(&s1)[ch];
                     *reinterpret_cast<float2*>(&ubuf[e]) = make_float2(v0, v1);
                 }
             }
@@ -442,14 +477,14 @@ __global__ __launch_bounds__(kThreads) void mfma_prefill_kernel(
     // stays float32
     auto split_x = [&](const f32x4 (&Xs)[2 * DM], bf16x8 (&XB)[DM][2]) {
 #pragma unroll
-        for (int q = 0; q < DM; ++q)
-#pragma unroll
-            for (int i = 0; i < 8; ++i) {
-                const float v = i < 4 ? Xs[q][i] : Xs[DM + q][i - 4];
-                const __bf16 a = static_cast<__bf16>(v);
-                XB[q][0][i] = a;
-                XB[q][1][i] = static_cast<__bf16>(v - static_cast<float>(a));
-            }
+        for (int q = 0; q < DM; ++q) {
+            const f32x4 re = Xs[q], im = Xs[DM + q];
+            const bf16x2 h0 = to_bf16x2(re[0], re[1]), h1 = to_bf16x2(re[2], re[3]);
+            const bf16x2 h2 = to_bf16x2(im[0], im[1]), h3 = to_bf16x2(im[2], im[3]);
+            XB[q][0] = concat4(h0, h1, h2, h3);
+            XB[q][1] = concat4(residual_bf16x2(re[0], re[1], h0), residual_bf16x2(re[2], re[3], h1),
+                               residual_bf16x2(im[0], im[1], h2), residual_bf16x2(im[2], im[3], h3));
+        }
     };
     // word of the y stage holding word dw (< SD) of (row, step)
     auto ysw = [&](int row, int step, int dw) { return row * RS + step * SD + (dw ^ ((step >> 2) & 3)); };
@@ -461,10 +496,9 @@ __global__ __launch_bounds__(kThreads) void mfma_prefill_kernel(
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
                 const int row = kN * bg + n, step = 16 * mt + 4 * g + i;
-                if constexpr (ES == 2 && CPW == 2) {
-                    const uint32_t lo = __builtin_bit_cast(uint16_t, static_cast<__bf16>(Y[0][mt][i]));
-                    const uint32_t hi = __builtin_bit_cast(uint16_t, static_cast<__bf16>(Y[1][mt][i]));
-                    ystage[ysw(row, step, w)] = lo | (hi << 16);
+                if constexpr (ES == 2 && CPW == 2) {  // channel 0 in the low half
+                    ystage[ysw(row, step, w)] =
+                        __builtin_bit_cast(uint32_t, to_bf16x2(Y[0][mt][i], Y[1][mt][i]));
                 } else if constexpr (ES == 2) {  // one bfloat16 channel: half word w % 2 of word w / 2
                     io_store(reinterpret_cast<IO*>(ystage) + 2 * ysw(row, step, w / 2) + w % 2,
                              Y[0][mt][i]);
@@ -619,24 +653,53 @@ __global__ __launch_bounds__(kThreads) void mfma_prefill_kernel(
     };
 
     // One full chunk kk: compute it from the staged tile, then (after the
-    // barrier) stage chunk kk + 1 from the registers it was loaded into one
-    // chunk earlier, write chunk kk's outputs and issue the loads of chunk
-    // kk + 2.  Loads and stores share one counter on this GPU, so the only
+    // barrier) stage chunk kk + 1 from the registers it was loaded into
+    // earlier, write chunk kk's outputs and issue the loads of chunk kk + 1 +
+    // PF.  Loads and stores share one counter on this GPU, so the only
     // outstanding accesses when the registers are consumed are the stores and
-    // loads issued a whole compute phase before.  The last, partial chunk is
-    // handled after the loop, so that the loop body holds no other path.
+    // loads issued at least a whole compute phase before.  The last, partial
+    // chunk is handled after the loop, so that the loop body holds no other
+    // path.
     const int64_t nfull = TL / kC;
-    load_tile(0);
-    store_tile(0);
-    if (nch > 1) load_tile(1);
-    lds_barrier();
-    for (int64_t kk = 0; kk < nfull; ++kk) {
-        compute_full();
-        lds_barrier();  // tile consumed, stage complete
-        if (kk + 1 < nch) store_tile(kk + 1);
-        if constexpr (MODE != kSegState) write_y(kk);
-        if (kk + 2 < nch) load_tile(kk + 2);
-        lds_barrier();  // next tile staged, stage free
+    if constexpr (PF == 1) {
+        load_tile(0, RA);
+        store_tile(0, RA);
+        if (nch > 1) load_tile(1, RA);
+        lds_barrier();
+        for (int64_t kk = 0; kk < nfull; ++kk) {
+            compute_full();
+            lds_barrier();  // tile consumed, stage complete
+            if (kk + 1 < nch) store_tile(kk + 1, RA);
+            if constexpr (MODE != kSegState) write_y(kk);
+            if (kk + 2 < nch) load_tile(kk + 2, RA);
+            lds_barrier();  // next tile staged, stage free
+        }
+    } else {
+        // two register tiles, A and B, alternating chunk by chunk (the loop
+        // is unrolled by two so that each has fixed registers).  The loads are
+        // issued on every path, past the end at the last chunk again, so that
+        // the number of accesses issued after each tile is the same on all
+        // paths and the wait for a tile leaves the next one in flight.
+        load_tile(0, RA);
+        load_tile(min(int64_t(1), nch - 1), RB);
+        store_tile(0, RA);
+        load_tile(min(int64_t(2), nch - 1), RA);
+        lds_barrier();
+        for (int64_t kk = 0; kk < nfull; kk += 2) {
+            compute_full();  // chunk kk; chunk kk + 1 in B, kk + 2 in A
+            lds_barrier();
+            if (kk + 1 < nch) store_tile(kk + 1, RB);
+            if constexpr (MODE != kSegState) write_y(kk);
+            load_tile(min(kk + 3, nch - 1), RB);
+            lds_barrier();
+            if (kk + 1 >= nfull) break;
+            compute_full();  // chunk kk + 1; chunk kk + 2 in A, kk + 3 in B
+            lds_barrier();
+            if (kk + 2 < nch) store_tile(kk + 2, RA);
+            if constexpr (MODE != kSegState) write_y(kk + 1);
+            load_tile(min(kk + 4, nch - 1), RA);
+            lds_barrier();
+        }
     }
     if constexpr (MODE == kWhole) {
         if (nch > nfull) {  // chunk nfull (staged); segmented launches have none
