@@ -274,10 +274,10 @@ constexpr int cpw_of()
 
 // Chunk tiles of u in flight while a chunk is computed (in registers, one
 // per tile): two where the registers allow it without spilling inside the
-// chunk loop (bfloat16 inputs with d = 16).  The waves of a workgroup run in
-// step through its barriers and there are only two per SIMD, so with one tile
-// in flight each chunk waits out a whole memory latency; a second tile hides
-// most of it.
+// chunk loop (bfloat16 inputs with d = 16).  There are only two waves per
+// SIMD, both of one workgroup and meeting at its barrier every chunk, so with
+// one tile in flight each chunk waits out most of a memory latency; a second
+// tile hides it.
 template <typename IO, int DM, int MODE>
 constexpr int pf_of()
 {
@@ -312,8 +312,12 @@ __global__ __launch_bounds__(kThreads) void mfma_prefill_kernel(
     constexpr int SD = CW * ES / 4;                   // words per (row, step)
     constexpr int RS = kC * SD + 4;                   // words per row
     constexpr int NYP = BN * kC * PPR;                // 16-byte output pieces per chunk
-    __shared__ __attribute__((aligned(16))) ST ubuf[CW * BN * US];
-    __shared__ __attribute__((aligned(16))) uint32_t ystage[MODE == kSegState ? 1 : BN * RS];
+    // u and y stages: one of each with one tile in flight; with two, two of
+    // each, so that a chunk's compute and the staging of its neighbours use
+    // different buffers and one barrier per chunk orders them
+    constexpr int PF = pf_of<IO, DM, MODE>();
+    __shared__ __attribute__((aligned(16))) ST ubuf[PF][CW * BN * US];
+    __shared__ __attribute__((aligned(16))) uint32_t ystage[PF][MODE == kSegState ? 1 : BN * RS];
     __shared__ __attribute__((aligned(16))) float2 lcs[CW][4][4 * DM];  // lambda^C per channel, lane group
 
     // ---- workgroup -> (channel group, batch group); logical index lin runs
@@ -400,8 +404,7 @@ __global__ __launch_bounds__(kThreads) void mfma_prefill_kernel(
         src0[j] = u + (int64_t(row_b(r)) * T + int64_t(row_k(r)) * TL + 2 * itp) * D +
                   min(c0 + ip * CPP, D - CPP);
     }
-    constexpr int PF = pf_of<IO, DM, MODE>();
-    uint4 RA[IPT][2], RB[PF == 2 ? IPT : 1][2];
+    uint4 RT[PF][IPT][2];  // u tiles in flight
     auto load_tile = [&](int64_t kk, auto& R0) {
         if ((kk + 1) * kC <= TL) {  // full chunk (uniform branch)
             const int64_t off = kk * kC * D;
@@ -424,7 +427,7 @@ __global__ __launch_bounds__(kThreads) void mfma_prefill_kernel(
             }
         }
     };
-    auto store_tile = [&](int64_t kk, const auto& R0) {
+    auto store_tile = [&](int64_t kk, const auto& R0, ST* ub) {
 #pragma unroll
         for (int j = 0; j < IPT; ++j) {
             if (tid + j * kThreads >= NITEM) continue;
@@ -441,25 +444,25 @@ __global__ __launch_bounds__(kThreads) void mfma_prefill_kernel(
                 if constexpr (ES == 2) {  // (step 2 itp, step 2 itp + 1) of channel ch
                     const uint32_t w0 = reinterpret_cast<const uint32_t*>(&s0)[ch / 2];
                     const uint32_t w1 = reinterpret_cast<const uint32_t*>(&s1)[ch / 2];
-                    reinterpret_cast<uint32_t*>(ubuf)[e / 2] =
+                    reinterpret_cast<uint32_t*>(ub)[e / 2] =
                         ch % 2 == 0 ? (w0 & 0xffffu) | (w1 << 16) : (w0 >> 16) | (w1 & 0xffff0000u);
                 } else {
                     const float v0 = reinterpret_cast<const float*>(&s0)[ch];
                     const float v1 = reinterpret_cast<const float*>(&s1)[ch];
-                    *reinterpret_cast<float2*>(&ubuf[e]) = make_float2(v0, v1);
+                    *reinterpret_cast<float2*>(&ub[e]) = make_float2(v0, v1);
                 }
             }
         }
     };
 
     // U operand of channel k, batch group bg: steps 8g..8g+7 of row 16 bg + n
-    auto load_u = [&](int k, int bg, bf16x8 (&U)[NTU]) {
+    auto load_u = [&](int k, int bg, bf16x8 (&U)[NTU], const ST* ub) {
         const int ue = ((w * CPW + k) * BN + kN * bg + n) * US + 8 * g;
         if constexpr (NTU == 1) {
-            U[0] = *reinterpret_cast<const bf16x8*>(&ubuf[ue]);
+            U[0] = *reinterpret_cast<const bf16x8*>(&ub[ue]);
         } else {
-            const float4 lo = *reinterpret_cast<const float4*>(&ubuf[ue]);
-            const float4 hi = *reinterpret_cast<const float4*>(&ubuf[ue + 4]);
+            const float4 lo = *reinterpret_cast<const float4*>(&ub[ue]);
+            const float4 hi = *reinterpret_cast<const float4*>(&ub[ue + 4]);
             const float uv[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
 #pragma unroll
             for (int i = 0; i < 8; ++i) {
@@ -490,20 +493,20 @@ __global__ __launch_bounds__(kThreads) void mfma_prefill_kernel(
     auto ysw = [&](int row, int step, int dw) { return row * RS + step * SD + (dw ^ ((step >> 2) & 3)); };
     // Y (row 16 bg + n, steps 16 mt + 4 g + i) of this wave's CPW channels
     // into the output stage, adjacent bfloat16 channels packed into one word
-    auto stage_y = [&](int bg, const f32x4 (&Y)[CPW][2]) {
+    auto stage_y = [&](int bg, const f32x4 (&Y)[CPW][2], uint32_t* ys) {
 #pragma unroll
         for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
                 const int row = kN * bg + n, step = 16 * mt + 4 * g + i;
                 if constexpr (ES == 2 && CPW == 2) {  // channel 0 in the low half
-                    ystage[ysw(row, step, w)] =
+                    ys[ysw(row, step, w)] =
                         __builtin_bit_cast(uint32_t, to_bf16x2(Y[0][mt][i], Y[1][mt][i]));
                 } else if constexpr (ES == 2) {  // one bfloat16 channel: half word w % 2 of word w / 2
-                    io_store(reinterpret_cast<IO*>(ystage) + 2 * ysw(row, step, w / 2) + w % 2,
+                    io_store(reinterpret_cast<IO*>(ys) + 2 * ysw(row, step, w / 2) + w % 2,
                              Y[0][mt][i]);
                 } else {
-                    reinterpret_cast<float*>(ystage)[ysw(row, step, w)] = Y[0][mt][i];
+                    reinterpret_cast<float*>(ys)[ysw(row, step, w)] = Y[0][mt][i];
                 }
             }
     };
@@ -516,7 +519,7 @@ __global__ __launch_bounds__(kThreads) void mfma_prefill_kernel(
     // full chunk, one batch group at a time: every product term is issued
     // for all independent accumulators of the wave's channels (2 Y tiles and
     // 2 DM S tiles per channel), then the carry and the output stage
-    auto compute_full = [&]() {
+    auto compute_full = [&](const ST* ub, uint32_t* ys) {
 #pragma unroll
         for (int bg = 0; bg < NBG; ++bg) {
             bf16x8 U[CPW][NTU];
@@ -524,7 +527,7 @@ __global__ __launch_bounds__(kThreads) void mfma_prefill_kernel(
             f32x4 Y[CPW][2], Sr[CPW][DM], Si[CPW][DM];
 #pragma unroll
             for (int k = 0; k < CPW; ++k) {
-                load_u(k, bg, U[k]);
+                load_u(k, bg, U[k], ub);
                 if constexpr (MODE != kSegState) split_x(X[k][bg], XB[k]);
                 Y[k][0] = Y[k][1] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -572,13 +575,13 @@ __global__ __launch_bounds__(kThreads) void mfma_prefill_kernel(
                         X[k][bg][q][i] = fmaf(l.x, xr, fmaf(-l.y, xi, Sr[k][q][i]));
                         X[k][bg][DM + q][i] = fmaf(l.x, xi, fmaf(l.y, xr, Si[k][q][i]));
                     }
-            if constexpr (MODE != kSegState) stage_y(bg, Y);
+            if constexpr (MODE != kSegState) stage_y(bg, Y, ys);
         }
     };
 
     // last, partial chunk of tr < C steps: outputs as above (the staged
     // inputs past T are zero), end state by the recurrence over its inputs
-    auto compute_partial = [&](int tr) {
+    auto compute_partial = [&](int tr, const ST* ub, uint32_t* ys) {
 #pragma unroll
         for (int bg = 0; bg < NBG; ++bg) {
             f32x4 Y[CPW][2];
@@ -586,7 +589,7 @@ __global__ __launch_bounds__(kThreads) void mfma_prefill_kernel(
             for (int k = 0; k < CPW; ++k) {
                 bf16x8 U[NTU];
                 bf16x8 XB[DM][2];
-                load_u(k, bg, U);
+                load_u(k, bg, U, ub);
                 split_x(X[k][bg], XB);
 #pragma unroll
                 for (int mt = 0; mt < 2; ++mt) {
@@ -604,7 +607,7 @@ __global__ __launch_bounds__(kThreads) void mfma_prefill_kernel(
                                             XB[q][kWXx[p]], Y[k][mt]);
                 }
             }
-            stage_y(bg, Y);
+            stage_y(bg, Y, ys);
         }
 #pragma unroll
         for (int k = 0; k < CPW; ++k) {
@@ -619,7 +622,7 @@ __global__ __launch_bounds__(kThreads) void mfma_prefill_kernel(
                         const float2 l1 = lam[int64_t(cc) * d + 16 * q + 4 * g + i];
                         float xr = X[k][bg][q][i], xi = X[k][bg][DM + q][i];
                         for (int j = 0; j < tr; ++j) {
-                            const float uv = static_cast<float>(ubuf[ue0 + j]);
+                            const float uv = static_cast<float>(ub[ue0 + j]);
                             const float nr = fmaf(l1.x, xr, fmaf(-l1.y, xi, uv));
                             xi = fmaf(l1.x, xi, l1.y * xr);
                             xr = nr;
@@ -633,7 +636,7 @@ __global__ __launch_bounds__(kThreads) void mfma_prefill_kernel(
 
     // stage -> y: piece r = row r / (kC PPR), step (r / PPR) % kC, channels
     // c0 + CPP (r % PPR) ..
-    auto write_y = [&](int64_t kk) {
+    auto write_y = [&](int64_t kk, const uint32_t* ys) {
         const int64_t t0 = kk * kC;
 #pragma unroll
         for (int j = 0; j < (NYP + kThreads - 1) / kThreads; ++j) {
@@ -641,7 +644,7 @@ __global__ __launch_bounds__(kThreads) void mfma_prefill_kernel(
             const int rp = r % PPR, rt = (r / PPR) % kC, rb = r / (PPR * kC);
             const int64_t gt = t0 + rt;
             if (r < NYP && b0 + rb < BV && gt < TL && c0 + rp * CPP < D) {
-                uint4 v = *reinterpret_cast<const uint4*>(&ystage[rb * RS + rt * SD + 4 * rp]);
+                uint4 v = *reinterpret_cast<const uint4*>(&ys[rb * RS + rt * SD + 4 * rp]);
                 const int f = (rt >> 2) & 3;  // undo the word permutation of the piece
                 if (f & 1) v = make_uint4(v.y, v.x, v.w, v.z);
                 if (f & 2) v = make_uint4(v.z, v.w, v.x, v.y);
@@ -652,60 +655,70 @@ __global__ __launch_bounds__(kThreads) void mfma_prefill_kernel(
         }
     };
 
-    // One full chunk kk: compute it from the staged tile, then (after the
-    // barrier) stage chunk kk + 1 from the registers it was loaded into
-    // earlier, write chunk kk's outputs and issue the loads of chunk kk + 1 +
-    // PF.  Loads and stores share one counter on this GPU, so the only
-    // outstanding accesses when the registers are consumed are the stores and
-    // loads issued at least a whole compute phase before.  The last, partial
-    // chunk is handled after the loop, so that the loop body holds no other
-    // path.
+    // One tile in flight (PF = 1): compute chunk kk from the staged tile,
+    // then (after a barrier) stage chunk kk + 1 from the registers it was
+    // loaded into one chunk earlier, write chunk kk's outputs and issue the
+    // loads of chunk kk + 2; a second barrier frees the stages.  Loads and
+    // stores share one counter on this GPU, so the only outstanding accesses
+    // when the registers are consumed are the stores and loads issued a whole
+    // compute phase before.
+    //
+    // Two tiles in flight (PF = 2): chunk kk is computed from u stage kk % 2
+    // into y stage kk % 2 while chunk kk + 1 goes from its register tile into
+    // the other u stage and chunk kk - 1's outputs leave the other y stage, so
+    // one barrier per chunk orders everything and the waves of a workgroup
+    // drift apart within it.  The register tiles and the stages alternate
+    // chunk by chunk (the loop is unrolled by two so that each has fixed
+    // registers and addresses); the tile that frees up takes the loads of
+    // chunk kk + 3.  These loads are issued on every path (past the end at the
+    // last chunks again) so that the number of accesses issued after each
+    // tile is the same on all paths and the wait for one tile leaves the other
+    // in flight.
+    //
+    // The last, partial chunk is handled after the loop, so that the loop
+    // body holds no other path.
     const int64_t nfull = TL / kC;
     if constexpr (PF == 1) {
-        load_tile(0, RA);
-        store_tile(0, RA);
-        if (nch > 1) load_tile(1, RA);
+        load_tile(0, RT[0]);
+        store_tile(0, RT[0], ubuf[0]);
+        if (nch > 1) load_tile(1, RT[0]);
         lds_barrier();
         for (int64_t kk = 0; kk < nfull; ++kk) {
-            compute_full();
+            compute_full(ubuf[0], ystage[0]);
             lds_barrier();  // tile consumed, stage complete
-            if (kk + 1 < nch) store_tile(kk + 1, RA);
-            if constexpr (MODE != kSegState) write_y(kk);
-            if (kk + 2 < nch) load_tile(kk + 2, RA);
+            if (kk + 1 < nch) store_tile(kk + 1, RT[0], ubuf[0]);
+            if constexpr (MODE != kSegState) write_y(kk, ystage[0]);
+            if (kk + 2 < nch) load_tile(kk + 2, RT[0]);
             lds_barrier();  // next tile staged, stage free
         }
     } else {
-        // two register tiles, A and B, alternating chunk by chunk (the loop
-        // is unrolled by two so that each has fixed registers).  The loads are
-        // issued on every path, past the end at the last chunk again, so that
-        // the number of accesses issued after each tile is the same on all
-        // paths and the wait for a tile leaves the next one in flight.
-        load_tile(0, RA);
-        load_tile(min(int64_t(1), nch - 1), RB);
-        store_tile(0, RA);
-        load_tile(min(int64_t(2), nch - 1), RA);
+        load_tile(0, RT[0]);
+        load_tile(min(int64_t(1), nch - 1), RT[1]);
+        store_tile(0, RT[0], ubuf[0]);
+        load_tile(min(int64_t(2), nch - 1), RT[0]);
         lds_barrier();
         for (int64_t kk = 0; kk < nfull; kk += 2) {
-            compute_full();  // chunk kk; chunk kk + 1 in B, kk + 2 in A
-            lds_barrier();
-            if (kk + 1 < nch) store_tile(kk + 1, RB);
-            if constexpr (MODE != kSegState) write_y(kk);
-            load_tile(min(kk + 3, nch - 1), RB);
+            compute_full(ubuf[0], ystage[0]);  // chunk kk; kk + 1 in RT[1], kk + 2 in RT[0]
+            if (kk + 1 < nch) store_tile(kk + 1, RT[1], ubuf[1]);
+            load_tile(min(kk + 3, nch - 1), RT[1]);
+            if constexpr (MODE != kSegState)
+                if (kk > 0) write_y(kk - 1, ystage[1]);
             lds_barrier();
             if (kk + 1 >= nfull) break;
-            compute_full();  // chunk kk + 1; chunk kk + 2 in A, kk + 3 in B
-            lds_barrier();
-            if (kk + 2 < nch) store_tile(kk + 2, RA);
-            if constexpr (MODE != kSegState) write_y(kk + 1);
-            load_tile(min(kk + 4, nch - 1), RA);
+            compute_full(ubuf[1], ystage[1]);  // chunk kk + 1; kk + 2 in RT[0], kk + 3 in RT[1]
+            if (kk + 2 < nch) store_tile(kk + 2, RT[0], ubuf[0]);
+            load_tile(min(kk + 4, nch - 1), RT[0]);
+            if constexpr (MODE != kSegState) write_y(kk, ystage[0]);
             lds_barrier();
         }
+        if constexpr (MODE != kSegState)
+            if (nfull > 0) write_y(nfull - 1, ystage[(nfull - 1) % 2]);
     }
     if constexpr (MODE == kWhole) {
         if (nch > nfull) {  // chunk nfull (staged); segmented launches have none
-            compute_partial(int(T - nfull * kC));
+            compute_partial(int(T - nfull * kC), ubuf[nfull % PF], ystage[nfull % PF]);
             lds_barrier();
-            write_y(nfull);
+            write_y(nfull, ystage[nfull % PF]);
         }
     }
 
