@@ -98,7 +98,8 @@ const char* lh_last_error(void);
 
 /*
  * Workspace bytes lh_prefill needs for these sizes and chunk length
- * (chunk_len as in lh_prefill).  Returns 0
+ * (chunk_len as in lh_prefill), for either input type (the larger of the
+ * float32 and bfloat16 plans' needs).  Returns 0
  * when the plan needs no workspace and (size_t)-1 when the arguments are
  * invalid.  Pure function of its arguments.
  */
@@ -124,10 +125,13 @@ size_t lh_prefill_workspace_bytes(int64_t B, int64_t D, int64_t d, int64_t T,
  *                   operands split into bfloat16 terms: three with float32
  *                   u/y, two with bfloat16 u/y; requires d = 16 or 32,
  *                   D % 8 == 0, T >= 1 and 16-byte aligned u and y, else
- *                   LH_ERR_INVALID_ARG).  The automatic plan uses the matrix
- *                   cores where supported and ceil(D/16) * ceil(B/32) >= 256
+ *                   LH_ERR_INVALID_ARG).  The automatic plan uses it where
+ *                   supported and either ceil(D/16) * ceil(B/32) >= 256
  *                   (enough workgroups to fill the GPU without splitting the
- *                   prompt in time);
+ *                   prompt in time) or an estimate of the chunk steps each
+ *                   compute unit walks puts it within 7/5 of the segmented
+ *                   plan below (the estimate depends on the input type, so
+ *                   float32 and bfloat16 calls may take different plans);
  *                   LH_PREFILL_MFMA_SEG = the segmented matrix-core plan: the
  *                   prompt is cut into 2^k segments of T / 2^k steps (a
  *                   multiple of 32, at least 256), the fewest whose (batch

@@ -204,7 +204,7 @@ size_t lh_prefill_workspace_bytes(int64_t B, int64_t D, int64_t d, int64_t T, in
 {
     if (check_sizes(B, D, d, T) != LH_OK || chunk_len < LH_PREFILL_MFMA_SEG) return (size_t)-1;
     lh::PrefillPlan p;
-    if (!lh::make_prefill_plan(B, D, d, T, chunk_len, &p)) return (size_t)-1;
+    if (!lh::make_prefill_plan(B, D, d, T, chunk_len, -1, &p)) return (size_t)-1;
     return p.ws_bytes;
 }
 
@@ -224,7 +224,7 @@ lh_status lh_prefill(const lh_c32* lambda, const lh_c32* R, const float* h0, con
                     "chunk_len must be >= 0, LH_PREFILL_MFMA or LH_PREFILL_MFMA_SEG");
     if ((s = check_dtype(io_dtype)) != LH_OK) return s;
     lh::PrefillPlan plan;
-    if (!lh::make_prefill_plan(B, D, d, T, chunk_len, &plan))
+    if (!lh::make_prefill_plan(B, D, d, T, chunk_len, io_dtype == LH_BF16 ? 1 : 0, &plan))
         return fail(LH_ERR_INVALID_ARG, "no prefill plan for these sizes%s",
                     chunk_len == LH_PREFILL_MFMA
                         ? " (the matrix-core plan needs d = 16 or 32, D % 8 == 0, T >= 1)"

@@ -51,8 +51,10 @@ struct PrefillPlan {
     size_t off_mfma;  // workspace offset of the matrix-core tables (segmented plan)
 };
 
-// Returns false when the sizes are invalid or overflow.
-bool make_prefill_plan(int64_t B, int64_t D, int64_t d, int64_t T, int64_t chunk_len,
+// Returns false when the sizes are invalid or overflow.  io: 0 float32, 1
+// bfloat16 u/y, -1 either (the automatic plan may differ between them; the
+// workspace size is then the larger of the two).
+bool make_prefill_plan(int64_t B, int64_t D, int64_t d, int64_t T, int64_t chunk_len, int io,
                        PrefillPlan* plan);
 
 // Launchers (asynchronous, on `stream`); they return the launch status.
@@ -63,7 +65,8 @@ hipError_t launch_prefill(const float2* lam, const float2* R, const float* h0,
 
 // Matrix-core prefill (d = 16 or 32, D a multiple of 8).
 bool mfma_supported(int64_t B, int64_t D, int64_t d, int64_t T);
-bool mfma_preferred(int64_t B, int64_t D, int64_t d);
+// Whether the automatic plan takes the whole-prompt matrix-core plan.
+bool mfma_preferred(int64_t B, int64_t D, int64_t d, int64_t T, bool bf16_io);
 size_t mfma_workspace_bytes(int64_t D, int64_t d);
 // Segment count of the segmented matrix-core plan (0 when T does not split
 // into segments of a multiple of 32 steps, at least 256 long).

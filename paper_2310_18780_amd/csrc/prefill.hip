@@ -287,9 +287,17 @@ inline bool grid_for(int64_t n, dim3* g)
 
 }  // namespace
 
-bool make_prefill_plan(int64_t B, int64_t D, int64_t d, int64_t T, int64_t chunk_len,
+bool make_prefill_plan(int64_t B, int64_t D, int64_t d, int64_t T, int64_t chunk_len, int io,
                        PrefillPlan* plan)
 {
+    if (io < 0) {  // workspace for either input type
+        PrefillPlan pb;
+        if (!make_prefill_plan(B, D, d, T, chunk_len, 0, plan) ||
+            !make_prefill_plan(B, D, d, T, chunk_len, 1, &pb))
+            return false;
+        if (pb.ws_bytes > plan->ws_bytes) plan->ws_bytes = pb.ws_bytes;
+        return true;
+    }
     if (B < 1 || D < 1 || d < 1 || d > 1024 || T < 0 || chunk_len < -2) return false;
     // element counts must fit comfortably in int64 (and the byte sizes too)
     const int64_t lim = INT64_C(1) << 58;
@@ -343,7 +351,7 @@ bool make_prefill_plan(int64_t B, int64_t D, int64_t d, int64_t T, int64_t chunk
     p.mfma_forced = chunk_len == -1 || chunk_len == -2;
     if (p.mfma_forced && !mfma_supported(B, D, d, T)) return false;
     p.mfma = chunk_len == -1 ||
-             (chunk_len == 0 && mfma_supported(B, D, d, T) && mfma_preferred(B, D, d));
+             (chunk_len == 0 && mfma_supported(B, D, d, T) && mfma_preferred(B, D, d, T, io == 1));
     p.mfma_seg = false;
     p.off_mfma = 0;
     if (p.mfma) {

@@ -273,15 +273,15 @@ constexpr int cpw_of()
 }
 
 // Chunk tiles of u in flight while a chunk is computed (in registers, one
-// per tile): two where the registers allow it without spilling inside the
-// chunk loop (bfloat16 inputs with d = 16).  There are only two waves per
-// SIMD, both of one workgroup and meeting at its barrier every chunk, so with
-// one tile in flight each chunk waits out most of a memory latency; a second
-// tile hides it.
+// per tile): two where the registers allow it without spilling (all but the
+// state-only pass and the float32 d = 32 whole-prompt kernel).  There are
+// only two waves per SIMD, both of one workgroup and meeting at its barrier
+// every chunk, so with one tile in flight each chunk waits out most of a
+// memory latency; a second tile hides it.
 template <typename IO, int DM, int MODE>
 constexpr int pf_of()
 {
-    return sizeof(IO) == 2 && DM == 1 && MODE != kSegState ? 2 : 1;
+    return MODE == kSegState || (sizeof(IO) == 4 && DM == 2 && MODE == kWhole) ? 1 : 2;
 }
 
 template <typename IO, int DM, int NBG, int MODE>
@@ -833,10 +833,38 @@ int64_t mfma_segments(int64_t B, int64_t D, int64_t T)
 // it when its workgroups alone fill the GPU, counted as 16 channels x 32 batch
 // rows (two rounds of the bfloat16 tiling with d = 16, 16 x 16).  The choice must not depend on the
 // input type, which the workspace query does not know.
-bool mfma_preferred(int64_t B, int64_t D, int64_t d)
+// Chunk steps of one pass on the busiest CU: its workgroups (one fits per
+// CU) run in rounds of kMinWorkgroups, each walking `chunks` chunks for NBG
+// groups of 16 columns.  rows = the pass's columns (batch rows, or (batch
+// row, segment) pairs).
+template <int MODE>
+int64_t pass_slots(int64_t rows, int64_t D, int64_t d, bool bf16_io, int64_t chunks)
 {
-    (void)d;
-    return ((D + 15) / 16) * ((B + 31) / 32) >= kMinWorkgroups;
+    const bool dm2 = d == 32;
+    const int cpw = bf16_io ? (dm2 ? cpw_of<bf16, 2, MODE>() : cpw_of<bf16, 1, MODE>())
+                            : (dm2 ? cpw_of<float, 2, MODE>() : cpw_of<float, 1, MODE>());
+    const int nbg = dm2 ? 1 : mfma_nbg(rows, d, bf16_io);
+    const int64_t cw = int64_t(kW) * cpw, bn = int64_t(kN) * nbg;
+    const int64_t wgs = (D + cw - 1) / cw * ((rows + bn - 1) / bn);
+    return (wgs + kMinWorkgroups - 1) / kMinWorkgroups * chunks * nbg;
+}
+
+bool mfma_preferred(int64_t B, int64_t D, int64_t d, int64_t T, bool bf16_io)
+{
+    if (((D + 15) / 16) * ((B + 31) / 32) >= kMinWorkgroups) return true;
+    // fewer columns: the whole-prompt plan against the segmented one by the
+    // chunk steps of their passes on the busiest CU (a chunk step costs about
+    // the same in every pass; the segmented plan also pays for its extra
+    // launches and second read of u, hence the 7/5 allowance, fitted to
+    // measured times of both plans over B = 1..64, D = 768 / 2048, d = 16 /
+    // 32, T = 1K..16K, float32 and bfloat16)
+    const int64_t nseg = mfma_segments(B, D, T);
+    if (nseg < 2) return false;
+    const int64_t seg_chunks = T / nseg / kC;
+    const int64_t whole = pass_slots<kWhole>(B, D, d, bf16_io, (T + kC - 1) / kC);
+    const int64_t seg = pass_slots<kSegState>(B * (nseg - 1), D, d, bf16_io, seg_chunks) +
+                        pass_slots<kSegOut>(B * nseg, D, d, bf16_io, seg_chunks);
+    return 5 * whole <= 7 * seg;
 }
 
 hipError_t launch_mfma_setup(const float2* lam, const float2* R, const float* h0, int64_t D,
