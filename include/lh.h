@@ -106,6 +106,24 @@ const char* lh_last_error(void);
 size_t lh_prefill_workspace_bytes(int64_t B, int64_t D, int64_t d, int64_t T,
                                   int64_t chunk_len);
 
+/* Prefill plans (what lh_prefill runs; see chunk_len there). */
+typedef enum {
+    LH_PLAN_SCAN = 0,      /* VALU scan: one sequential pass or parallel time chunks */
+    LH_PLAN_MFMA = 1,      /* matrix-core plan over the whole prompt */
+    LH_PLAN_MFMA_SEG = 2   /* segmented matrix-core plan */
+} lh_prefill_plan_kind;
+
+/*
+ * The plan lh_prefill takes for these sizes, chunk length and input type
+ * when u and y are 16-byte aligned (automatic matrix-core plans run the VALU
+ * scan, with the same workspace, when they are not).  Returns an
+ * lh_prefill_plan_kind, or -1 when the arguments are invalid or no plan
+ * exists (as lh_prefill would fail).  Pure function of its arguments; host
+ * only, no device call.
+ */
+int lh_prefill_plan(int64_t B, int64_t D, int64_t d, int64_t T, int64_t chunk_len,
+                    lh_dtype io_dtype);
+
 /*
  * Prefill: outputs y[b,t,c] for t < T and the post-prompt state
  * state[b,c,n] = x_T (Sec. 3.4, "fast pre-filling"; states start at x_0 = 0).

@@ -87,6 +87,8 @@ def lib() -> ctypes.CDLL:
     L.lh_last_error.restype = ctypes.c_char_p
     L.lh_prefill_workspace_bytes.argtypes = [i64, i64, i64, i64, i64]
     L.lh_prefill_workspace_bytes.restype = sz
+    L.lh_prefill_plan.argtypes = [i64, i64, i64, i64, i64, ctypes.c_int]
+    L.lh_prefill_plan.restype = ctypes.c_int
     L.lh_prefill.argtypes = [vp, vp, vp, vp, i64, i64, i64, i64, ctypes.c_int, vp, vp, i64, vp,
                              sz, vp]
     L.lh_prefill.restype = ctypes.c_int
@@ -123,6 +125,18 @@ def workspace_bytes(B: int, D: int, d: int, T: int, chunk_len: int = 0) -> int:
     if n == ctypes.c_size_t(-1).value:
         raise LHError(1, f"invalid sizes B={B} D={D} d={d} T={T} chunk_len={chunk_len}")
     return int(n)
+
+
+PREFILL_PLANS = ("scan", "mfma", "mfma_seg")
+
+
+def prefill_plan(B: int, D: int, d: int, T: int, chunk_len: int = 0, io: str = "f32") -> str:
+    """The plan ``prefill`` takes for 16-byte aligned u and y (``lh_prefill_plan``):
+    "scan" (VALU), "mfma" (matrix cores, whole prompt) or "mfma_seg" (segmented)."""
+    k = lib().lh_prefill_plan(B, D, d, T, chunk_len, {"f32": 0, "bf16": 1}[io])
+    if k < 0:
+        raise LHError(1, f"no prefill plan for B={B} D={D} d={d} T={T} chunk_len={chunk_len} io={io}")
+    return PREFILL_PLANS[k]
 
 
 def _io_dtype(t) -> int:

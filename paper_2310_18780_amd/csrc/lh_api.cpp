@@ -208,6 +208,17 @@ size_t lh_prefill_workspace_bytes(int64_t B, int64_t D, int64_t d, int64_t T, in
     return p.ws_bytes;
 }
 
+int lh_prefill_plan(int64_t B, int64_t D, int64_t d, int64_t T, int64_t chunk_len,
+                    lh_dtype io_dtype)
+{
+    if (check_sizes(B, D, d, T) != LH_OK || chunk_len < LH_PREFILL_MFMA_SEG ||
+        (io_dtype != LH_F32 && io_dtype != LH_BF16))
+        return -1;
+    lh::PrefillPlan p;
+    if (!lh::make_prefill_plan(B, D, d, T, chunk_len, io_dtype == LH_BF16 ? 1 : 0, &p)) return -1;
+    return p.mfma_seg ? LH_PLAN_MFMA_SEG : p.mfma ? LH_PLAN_MFMA : LH_PLAN_SCAN;
+}
+
 lh_status lh_prefill(const lh_c32* lambda, const lh_c32* R, const float* h0, const void* u,
                      int64_t B, int64_t D, int64_t d, int64_t T, lh_dtype io_dtype,
                      lh_c32* state, void* y, int64_t chunk_len, void* workspace,

@@ -108,6 +108,27 @@ def test_workspace_sizes():
         assert L.lh_prefill_workspace_bytes(*args) == bad, args
 
 
+def test_prefill_plan_query():
+    """lh_prefill_plan: the plan lh_prefill takes (host only, no device)."""
+    P = lh.prefill_plan
+    assert P(1, 4, 4, 64) == "scan"                    # d = 4: no matrix-core plan
+    assert P(256, 2048, 64, 1024) == "scan"            # d = 64
+    assert P(64, 2048, 16, 4096, io="bf16") == "mfma"  # enough (channel, row) tiles
+    assert P(4, 1024, 32, 65536) == "mfma_seg"         # 4 rows, long prompt
+    assert P(16, 768, 16, 2048) == "mfma"              # chunk-step estimate: whole prompt
+    assert P(2, 512, 32, 8192) == "mfma_seg"           # chunk-step estimate: segments
+    assert P(2, 70, 16, 300) == "scan"                 # D % 8 != 0
+    assert P(4, 1024, 32, 500) == "scan"               # T does not split into segments
+    # explicit plans
+    assert P(4, 1024, 32, 65536, chunk_len=2048) == "scan"
+    assert P(2, 16, 16, 64, chunk_len=-1) == "mfma"
+    assert P(2, 16, 16, 1024, chunk_len=-2) == "mfma_seg"
+    L = lh.lib()
+    for args in [(2, 12, 16, 64, -1, 0), (4, 1024, 32, 500, -2, 0), (0, 1, 1, 1, 0, 0),
+                 (1, 1, 1, 1, -3, 0), (1, 1, 1, 1, 0, 2), (1, 1, 1, -1, 0, 1)]:
+        assert L.lh_prefill_plan(*args) == -1, args
+
+
 # made-up, well-separated, aligned addresses (never dereferenced)
 A = 0x7F0000000000
 MB = 1 << 20

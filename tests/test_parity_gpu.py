@@ -329,3 +329,32 @@ def test_unaligned_io_falls_back_to_the_vector_scan(io):
         yp = _np(y).transpose(0, 2, 1).reshape(B * D, T)
         check_y(yp, ref["y_prefill"].transpose(0, 2, 1).reshape(B * D, T), io, "unaligned prefill y")
         check_x(_np(state).reshape(-1, d), ref["x_T"].reshape(-1, d), "unaligned prefill x_T")
+
+
+@pytest.mark.parametrize("case", [
+    # (B, D, d, T, io, plan the automatic choice must equal)
+    (16, 768, 16, 2048, "f32", -1),  # the 768-wide workload: the whole-prompt plan
+    (2, 512, 32, 8192, "f32", -2),   # few rows, long prompt: the segmented plan
+    (2, 512, 16, 8192, "bf16", -2),
+    (64, 2048, 16, 256, "bf16", -1),
+])
+def test_automatic_plan_choice(case):
+    """The automatic plan's outputs and state equal, bit for bit, those of the
+    matrix-core plan its chunk-step estimate picks (whole prompt or
+    segmented) for these shapes."""
+    import torch
+
+    import paper_2310_18780_amd as lh
+
+    B, D, d, T, io, want = case
+    assert lh.prefill_plan(B, D, d, T, io=io) == {-1: "mfma", -2: "mfma_seg"}[want]
+    w, (lam, R, h0, up, ud) = small_case(B, D, d, T, 0, io)
+    t = to_device(lam, R, h0, up, ud, io)
+    res = {}
+    for ch in (0, want):
+        y = torch.full_like(t["u"], float("nan"))
+        st = torch.full((B, D, d), complex(float("nan"), 0), dtype=torch.complex64, device="cuda")
+        lh.prefill(t["lam"], t["R"], t["h0"], t["u"], st, y, chunk_len=ch)
+        torch.cuda.synchronize()
+        res[ch] = (y, st)
+    assert torch.equal(res[0][0], res[want][0]) and torch.equal(res[0][1], res[want][1])
