@@ -86,6 +86,9 @@ SMALL = [
     (2, 16, 16, 32, 3, "bf16", -1),    # one full chunk, nothing after it
     (3, 24, 16, 33, 3, "bf16", -1),    # one full chunk and a partial one
     (2, 16, 16, 96, 3, "bf16", -1),    # three full chunks (odd count, no partial)
+    (3, 16, 16, 20, 3, "f32", -1),     # float32: only a partial chunk
+    (2, 24, 16, 96, 3, "f32", -1),     # float32: three full chunks
+    (20, 16, 16, 33, 3, "f32", -1),    # float32, 2 batch groups per wave: a full and a partial chunk
     (5, 67, 2, 33, 6, "bf16", 0),      # d = 2: one lane per row, B not a multiple of 4
     (3, 1, 16, 90, 5, "f32", 0),       # a single channel
     (2, 1, 5, 70, 4, "bf16", 16),      # a single channel, chunked, generic decode
@@ -97,6 +100,7 @@ SMALL = [
     (5, 40, 32, 4096, 3, "bf16", -2),  # d = 32, bfloat16, 16 segments, 5 rows
     (40, 16, 16, 1024, 3, "f32", -2),  # 2 column groups per wave (float32, d = 16)
     (2, 24, 16, 576, 3, "bf16", -2),   # two segments of 9 chunks (odd count), bfloat16
+    (2, 24, 32, 576, 3, "f32", -2),    # the same with float32, d = 32
 ]
 
 
