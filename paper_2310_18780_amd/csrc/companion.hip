@@ -285,21 +285,30 @@ hipError_t step_io(const double* a, const double* beta, const float* h0, double*
                    const void* u_t, void* y_t, int64_t B, int64_t D, int64_t d, hipStream_t s)
 {
     const int64_t per_block = kThreads / next_pow2(static_cast<int>(d));  // channels per block
-    const int64_t gx = (D + per_block - 1) / per_block, gy = (B + kRows - 1) / kRows;
-    if (gx > 0x7fffffff || gy > 0xffff) return hipErrorInvalidConfiguration;
-    const dim3 g(static_cast<uint32_t>(gx), static_cast<uint32_t>(gy));
-    switch (2 * d) {
+    const int64_t gx = (D + per_block - 1) / per_block;
+    if (gx > 0x7fffffff) return hipErrorInvalidConfiguration;
+    // batch rows in slices of at most 65535 row groups (the grid's y limit)
+    constexpr int64_t kSlice = INT64_C(0xffff) * kRows;
+    for (int64_t b0 = 0; b0 < B; b0 += kSlice) {
+        const int64_t nb = B - b0 < kSlice ? B - b0 : kSlice;
+        const dim3 g(static_cast<uint32_t>(gx), static_cast<uint32_t>((nb + kRows - 1) / kRows));
+        double* st = state + b0 * D * 2 * d;
+        const IO* uu = static_cast<const IO*>(u_t) + b0 * D;
+        IO* yy = static_cast<IO*>(y_t) + b0 * D;
+        switch (2 * d) {
 #define LH_CASE(O)                                                                              \
     case O:                                                                                     \
         hipLaunchKernelGGL((companion_step_kernel<IO, O>), g, dim3(kThreads), 0, s, a, beta,    \
-                           h0, state, static_cast<const IO*>(u_t), static_cast<IO*>(y_t), B,    \
-                           D);                                                                  \
+                           h0, st, uu, yy, nb, D);                                              \
         break;
-        LH_COMPANION_ORDERS(LH_CASE)
+            LH_COMPANION_ORDERS(LH_CASE)
 #undef LH_CASE
-        default: return hipErrorInvalidValue;
+            default: return hipErrorInvalidValue;
+        }
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
     }
-    return hipGetLastError();
+    return hipSuccess;
 }
 
 template <typename IO>

@@ -189,3 +189,41 @@ def test_matches_modal_decode_on_a_workload():
     d_ = (yc - ym).abs().amax(dim=0)
     m_ = ym.abs().amax(dim=0)
     assert bool(torch.all(d_ <= 2e-4 * m_)), float((d_ / m_).max())
+
+
+def test_batch_past_the_grid_limit():
+    """B = 4 * 65535 + 1 rows: the step runs in two launches (65535 row groups
+    of 4, then one row); sampled rows, including both sides of the cut,
+    against the oracle's companion recurrence and modal outputs."""
+    import torch
+
+    import paper_2310_18780_amd as lh
+
+    B, D, d, T0, K = 4 * 65535 + 1, 1, 1, 3, 2
+    w = workloads.Workload("case", B, D, d, T0, K, "f32", 0.5, 0.95, np.pi, 1.0, 0)
+    lam, R, h0 = workloads.make_params(w)
+    rng = np.random.default_rng(12)
+    up = rng.standard_normal((B, T0, D)).astype(np.float32)
+    ud = rng.standard_normal((B, K, D)).astype(np.float32)
+    a, beta = gpu_coeffs(lam, R)
+    ar, br, b0 = oc.from_modal(lam, R, h0)
+    state = torch.full((B, D, 2 * d), float("nan"), dtype=torch.float64, device="cuda")
+    lh.companion_init(a, torch.from_numpy(up).cuda(), state)
+    h0_t = torch.from_numpy(h0).cuda()
+    ud_t = torch.from_numpy(np.ascontiguousarray(ud.transpose(1, 0, 2))).cuda()
+    y = torch.full((K, B, D), float("nan"), device="cuda")
+    for k in range(K):
+        lh.companion_step(a, beta, h0_t, state, ud_t[k], y[k])
+    torch.cuda.synchronize()
+    cut = 4 * 65535
+    bs = sorted({0, 1, cut - 2, cut - 1, cut, *rng.integers(B, size=100).tolist()})
+    xe = state[bs, 0].cpu().numpy()
+    yg = y[:, bs, 0].cpu().numpy().T
+    xr = np.empty_like(xe)
+    for i, b in enumerate(bs):
+        x0 = oc.fast_init(ar[0], up[b, :, 0])
+        _, xr[i] = oc.companion_run(ar[0], br[0], b0[0], ud[b, :, 0], x0)
+    check_state(xe, xr, "state after the steps")
+    ref = oracle.run_rows(lam, R, h0, up, ud, [(b, 0) for b in bs])
+    e = check_y(yg, ref["y_dec"], "f32", "companion decode y")
+    _log(f"[companion grid limit] max row-relative output error {e:.2e}")

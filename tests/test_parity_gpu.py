@@ -362,3 +362,30 @@ def test_automatic_plan_choice(case):
         torch.cuda.synchronize()
         res[ch] = (y, st)
     assert torch.equal(res[0][0], res[want][0]) and torch.equal(res[0][1], res[want][1])
+
+
+def test_batch_past_the_grid_limit():
+    """B = 4 * 65535 + 1 rows: the decode step's fast path would need 65536
+    row groups in the grid's y dimension, so the step takes the generic path;
+    B = 4 * 65535 is the largest fast-path batch.  Sampled rows (both ends and
+    the rows around the row-group boundaries) against the oracle."""
+    import torch
+
+    import paper_2310_18780_amd as lh
+
+    for B in (4 * 65535, 4 * 65535 + 1):
+        D, d, T, K = 1, 2, 3, 2
+        w = workloads.Workload("case", B, D, d, T, K, "f32", 0.5, 0.999, np.pi, 1.0 / d, 0)
+        lam, R, h0 = workloads.make_params(w)
+        rng = np.random.default_rng(11)
+        up = rng.standard_normal((B, T, D)).astype(np.float32)
+        ud = rng.standard_normal((B, K, D)).astype(np.float32)
+        out = run_gpu(to_device(lam, R, h0, up, ud, "f32"))
+        bs = sorted({0, 1, 2, 3, 4, B - 5, B - 4, B - 3, B - 2, B - 1,
+                     *rng.integers(B, size=200).tolist()})
+        rows = [(b, 0) for b in bs]
+        got = gather_rows(out, rows)
+        del out
+        torch.cuda.empty_cache()
+        ref = oracle.run_rows(lam, R, h0, up, ud, rows)
+        _log(f"[grid limit] B={B} errors {compare_rows(got, ref, 'f32')}")
