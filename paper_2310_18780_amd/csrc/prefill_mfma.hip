@@ -43,9 +43,10 @@
 // permuted to match (K index 8g + i <-> the lane's rows).  A workgroup is 8
 // waves = 8 CPW consecutive channels.  The u tile of a chunk is staged
 // through LDS (transposed to [channel][row][step]) from registers loaded one
-// chunk ahead; the outputs go back through LDS so that every global access is
-// a 16-byte piece of a whole (row, step) segment of the workgroup's channels.
-// Barriers order LDS only, so the prefetch stays in flight across them.
+// or two chunks ahead (pf_of); the outputs go back through LDS so that every
+// global access is a 16-byte piece of a whole (row, step) segment of the
+// workgroup's channels.  Barriers order LDS only, so the prefetch stays in
+// flight across them.
 // Workgroups are ordered so that the channel groups sharing 128-byte lines
 // of u and y run on one XCD (workgroup i runs on XCD i mod 8).
 //
