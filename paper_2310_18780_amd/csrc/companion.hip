@@ -34,6 +34,9 @@ namespace {
 constexpr int kMaxOrd = 2 * kCompanionMaxModes;
 constexpr int kThreads = 256;
 constexpr int kBlk = 8;  // initialisation: steps per prefetched block
+// initialisation: batch rows per thread (sharing the taps); one for the
+// largest orders, whose accumulators would not fit twice in registers
+__host__ __device__ constexpr int init_rows(int ord) { return ord <= 16 ? 2 : 1; }
 
 // One 64-thread workgroup per channel; thread k owns the coefficient of w^k.
 __global__ __launch_bounds__(64) void companion_coeffs_kernel(const float2* __restrict__ lam,
@@ -197,28 +200,40 @@ __global__ __launch_bounds__(kThreads) void companion_g_kernel(const double* __r
     }
 }
 
-// state[b, c, j] = v_{T-1-j} = sum_{k <= T-1-j} g_{T-1-j-k} u_k, one thread per
-// (b, c); a window of the 2d taps g_{T-1-j-k} slides along k.
+// state[b, c, j] = v_{T-1-j} = sum_{k <= T-1-j} g_{T-1-j-k} u_k: one thread
+// per channel c and group of init_rows(2d) batch rows, which share the window of
+// the 2d taps g_{T-1-j-k} sliding along k (one tap load per step for all the
+// rows).
 template <typename IO, int ORD>
 __global__ __launch_bounds__(kThreads) void companion_init_kernel(const double* __restrict__ g,
                                                                  const IO* __restrict__ u,
                                                                  int64_t B, int64_t D, int64_t T,
                                                                  double* __restrict__ state)
 {
+    constexpr int NR = init_rows(ORD);
     const int64_t i = int64_t(blockIdx.x) * kThreads + threadIdx.x;
-    if (i >= B * D) return;
-    const int64_t b = i / D, c = i % D;
-    const IO* ub = u + b * T * D + c;
-    double win[ORD], acc[ORD];
+    const int64_t nbg = (B + NR - 1) / NR;
+    if (i >= nbg * D) return;
+    const int64_t bg = i / D, c = i % D;
+    const IO* ub[NR];
+#pragma unroll
+    for (int r = 0; r < NR; ++r) {
+        const int64_t b = bg * NR + r < B ? bg * NR + r : B - 1;  // loads stay in bounds
+        ub[r] = u + b * T * D + c;
+    }
+    double win[ORD], acc[NR][ORD];
 #pragma unroll
     for (int j = 0; j < ORD; ++j) {
         win[j] = T - 1 - j >= 0 ? g[(T - 1 - j) * D + c] : 0.0;
-        acc[j] = 0.0;
+#pragma unroll
+        for (int r = 0; r < NR; ++r) acc[r][j] = 0.0;
     }
     // one step k: accumulate, then slide the window (next tap g_{T-1-2d-k})
-    auto step = [&](double uk, double gnext) {
+    auto step = [&](const double (&uk)[NR], double gnext) {
 #pragma unroll
-        for (int j = 0; j < ORD; ++j) acc[j] = fma(win[j], uk, acc[j]);
+        for (int j = 0; j < ORD; ++j)
+#pragma unroll
+            for (int r = 0; r < NR; ++r) acc[r][j] = fma(win[j], uk[r], acc[r][j]);
 #pragma unroll
         for (int j = 0; j < ORD - 1; ++j) win[j] = win[j + 1];
         win[ORD - 1] = gnext;
@@ -227,18 +242,19 @@ __global__ __launch_bounds__(kThreads) void companion_init_kernel(const double* 
     // blocks of kBlk steps, the next block's inputs loaded while the current
     // one is used (two buffers in turn), then the remaining steps
     const int64_t nblk = T / kBlk;
-    double ua[kBlk], ga[kBlk], ub2[kBlk], gb[kBlk];
-    auto load = [&](double (&uu)[kBlk], double (&gg)[kBlk], int64_t k0) {
+    double ua[kBlk][NR], ga[kBlk], ub2[kBlk][NR], gb[kBlk];
+    auto load = [&](double (&uu)[kBlk][NR], double (&gg)[kBlk], int64_t k0) {
 #pragma unroll
         for (int s2 = 0; s2 < kBlk; ++s2) {
-            uu[s2] = io_load(ub + (k0 + s2) * D);
+#pragma unroll
+            for (int r = 0; r < NR; ++r) uu[s2][r] = io_load(ub[r] + (k0 + s2) * D);
             gg[s2] = gtap(k0 + s2);
         }
         // keep the loads here, ahead of the arithmetic that follows
         asm volatile("" ::: "memory");
         __builtin_amdgcn_sched_barrier(0);
     };
-    auto use = [&](const double (&uu)[kBlk], const double (&gg)[kBlk]) {
+    auto use = [&](const double (&uu)[kBlk][NR], const double (&gg)[kBlk]) {
 #pragma unroll
         for (int s2 = 0; s2 < kBlk; ++s2) step(uu[s2], gg[s2]);
     };
@@ -256,10 +272,20 @@ __global__ __launch_bounds__(kThreads) void companion_init_kernel(const double* 
             k += kBlk;
         }
     }
-    for (; k < T; ++k) step(io_load(ub + k * D), gtap(k));
-    double2* xs = reinterpret_cast<double2*>(state + i * ORD);
+    for (; k < T; ++k) {
+        double uk[NR];
 #pragma unroll
-    for (int m = 0; m < ORD / 2; ++m) xs[m] = make_double2(acc[2 * m], acc[2 * m + 1]);
+        for (int r = 0; r < NR; ++r) uk[r] = io_load(ub[r] + k * D);
+        step(uk, gtap(k));
+    }
+#pragma unroll
+    for (int r = 0; r < NR; ++r) {
+        const int64_t b = bg * NR + r;
+        if (b >= B) break;
+        double2* xs = reinterpret_cast<double2*>(state + (b * D + c) * ORD);
+#pragma unroll
+        for (int m = 0; m < ORD / 2; ++m) xs[m] = make_double2(acc[r][2 * m], acc[r][2 * m + 1]);
+    }
 }
 
 __global__ __launch_bounds__(kThreads) void companion_zero_kernel(double* __restrict__ p,
@@ -316,7 +342,8 @@ hipError_t init_io(const double* a, const void* u, int64_t B, int64_t D, int64_t
                    double* state, double* gbuf, hipStream_t s)
 {
     uint32_t gc, gr;
-    if (!blocks(D, &gc) || !blocks(B * D, &gr)) return hipErrorInvalidConfiguration;
+    const int nr = init_rows(static_cast<int>(2 * d));
+    if (!blocks(D, &gc) || !blocks((B + nr - 1) / nr * D, &gr)) return hipErrorInvalidConfiguration;
     hipError_t e;
     switch (2 * d) {
 #define LH_CASE(O)                                                                               \
