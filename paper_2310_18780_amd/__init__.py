@@ -6,6 +6,7 @@ calls the library.  Every step of the computation runs in the library's HIP
 kernels; there is no fallback.  PyTorch provides device memory and streams.
 
     prefill(lam, R, h0, u, state, y)   # y[b,t,c], t < T, and state = x_T
+    prefill_plan(B, D, d, T, io="bf16")  # which plan prefill takes ("scan", "mfma", "mfma_seg")
     prefill_fft(lam, R, h0, u, state, y)  # the same results by FFT convolution
     step(lam, R, h0, state, u_t, y_t)  # y_t from x_t, then x_{t+1} in place
 
@@ -26,6 +27,8 @@ __all__ = [
     "lib",
     "library_path",
     "workspace_bytes",
+    "prefill_plan",
+    "PREFILL_PLANS",
     "prefill",
     "fft_workspace_bytes",
     "prefill_fft",
