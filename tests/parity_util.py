@@ -118,6 +118,23 @@ def check_x(x_gpu: np.ndarray, x_ref: np.ndarray, what: str):
     return float(np.max(err / np.maximum(rowmax, 1e-300))) if err.size else 0.0
 
 
+def _report(pairs) -> Dict[str, float]:
+    """Reported beside the row checks (not asserted): the global relative l2
+    error of each result and its worst elementwise error relative to
+    max(|ref|, 1e-3 * max |ref|) (an absolute floor at 1e-3 of the scale)."""
+    out = {}
+    for name, g, r in pairs:
+        g = np.asarray(g).astype(np.complex128 if np.iscomplexobj(g) else np.float64)
+        r = np.asarray(r)
+        if r.size == 0:
+            continue
+        den = np.linalg.norm(r.ravel())
+        out[f"l2_{name}"] = float(np.linalg.norm((g - r).ravel()) / den) if den > 0 else 0.0
+        floor = 1e-3 * np.max(np.abs(r))
+        out[f"elem_{name}"] = float(np.max(np.abs(g - r) / np.maximum(np.abs(r), max(floor, 1e-300))))
+    return out
+
+
 def compare_full(out, ref, io: str) -> Dict[str, float]:
     """Every output and state of a small case."""
     B, T, D = out["y_prefill"].shape
@@ -127,12 +144,16 @@ def compare_full(out, ref, io: str) -> Dict[str, float]:
     r_yd = ref["y_dec"].transpose(0, 2, 1).reshape(B * D, -1)
     d = out["x_T"].shape[-1]
     rm = seq_rowmax(r_yp, r_yd)
-    return dict(
+    xT, xe = _np(out["x_T"]).reshape(-1, d), _np(out["x_end"]).reshape(-1, d)
+    res = dict(
         y_prefill=check_y(yp, r_yp, io, "prefill y", rowmax=rm),
         y_dec=check_y(yd, r_yd, io, "decode y", rowmax=rm),
-        x_T=check_x(_np(out["x_T"]).reshape(-1, d), ref["x_T"].reshape(-1, d), "x_T"),
-        x_end=check_x(_np(out["x_end"]).reshape(-1, d), ref["x_end"].reshape(-1, d), "x_end"),
+        x_T=check_x(xT, ref["x_T"].reshape(-1, d), "x_T"),
+        x_end=check_x(xe, ref["x_end"].reshape(-1, d), "x_end"),
     )
+    res.update(_report([("y_prefill", yp, r_yp), ("y_dec", yd, r_yd),
+                        ("x_T", xT, ref["x_T"].reshape(-1, d)), ("x_end", xe, ref["x_end"].reshape(-1, d))]))
+    return res
 
 
 def gather_rows(out, rows: Sequence[Tuple[int, int]]):
@@ -151,12 +172,14 @@ def gather_rows(out, rows: Sequence[Tuple[int, int]]):
 
 def compare_rows(got, ref, io: str) -> Dict[str, float]:
     rm = seq_rowmax(ref["y_prefill"], ref["y_dec"])
-    return dict(
+    res = dict(
         y_prefill=check_y(got["y_prefill"], ref["y_prefill"], io, "prefill y", rowmax=rm),
         y_dec=check_y(got["y_dec"], ref["y_dec"], io, "decode y", rowmax=rm),
         x_T=check_x(got["x_T"], ref["x_T"], "x_T"),
         x_end=check_x(got["x_end"], ref["x_end"], "x_end"),
     )
+    res.update(_report([(k, got[k], ref[k]) for k in ("y_prefill", "y_dec", "x_T", "x_end")]))
+    return res
 
 
 def sample_rows(B: int, D: int, n: int, seed: int = 123) -> List[Tuple[int, int]]:
