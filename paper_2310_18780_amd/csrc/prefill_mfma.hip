@@ -664,17 +664,16 @@ __global__ __launch_bounds__(kThreads) void mfma_prefill_kernel(
     // when the registers are consumed are the stores and loads issued a whole
     // compute phase before.
     //
-    // Two tiles in flight (PF = 2): chunk kk is computed from u stage kk % 2
-    // into y stage kk % 2 while chunk kk + 1 goes from its register tile into
-    // the other u stage and chunk kk - 1's outputs leave the other y stage, so
+    // PF >= 2 tiles in flight: chunk kk is computed from u stage kk % PF into
+    // y stage kk % PF while chunk kk + 1 goes from its register tile into the
+    // next u stage and chunk kk - 1's outputs leave the previous y stage, so
     // one barrier per chunk orders everything and the waves of a workgroup
-    // drift apart within it.  The register tiles and the stages alternate
-    // chunk by chunk (the loop is unrolled by two so that each has fixed
-    // registers and addresses); the tile that frees up takes the loads of
-    // chunk kk + 3.  These loads are issued on every path (past the end at the
-    // last chunks again) so that the number of accesses issued after each
-    // tile is the same on all paths and the wait for one tile leaves the other
-    // in flight.
+    // drift apart within it.  Tile t lives in register slot t % PF (the loop
+    // is unrolled by PF so that slots and stages have fixed registers and
+    // addresses); the slot that frees up takes the loads of chunk kk + 1 + PF.
+    // These loads are issued on every path (past the end at the last chunks
+    // again) so that the number of accesses issued after each tile is the same
+    // on all paths and the wait for one tile leaves the others in flight.
     //
     // The last, partial chunk is handled after the loop, so that the loop
     // body holds no other path.
@@ -693,27 +692,28 @@ __global__ __launch_bounds__(kThreads) void mfma_prefill_kernel(
             lds_barrier();  // next tile staged, stage free
         }
     } else {
-        load_tile(0, RT[0]);
-        load_tile(min(int64_t(1), nch - 1), RT[1]);
+        // tile t lives in register slot t % PF; chunk kk uses stage kk % PF
+#pragma unroll
+        for (int q = 0; q < PF; ++q) load_tile(min(int64_t(q), nch - 1), RT[q]);
         store_tile(0, RT[0], ubuf[0]);
-        load_tile(min(int64_t(2), nch - 1), RT[0]);
+        load_tile(min(int64_t(PF), nch - 1), RT[0]);
         lds_barrier();
-        for (int64_t kk = 0; kk < nfull; kk += 2) {
-            compute_full(ubuf[0], ystage[0]);  // chunk kk; kk + 1 in RT[1], kk + 2 in RT[0]
-            if (kk + 1 < nch) store_tile(kk + 1, RT[1], ubuf[1]);
-            load_tile(min(kk + 3, nch - 1), RT[1]);
-            if constexpr (MODE != kSegState)
-                if (kk > 0) write_y(kk - 1, ystage[1]);
-            lds_barrier();
-            if (kk + 1 >= nfull) break;
-            compute_full(ubuf[1], ystage[1]);  // chunk kk + 1; kk + 2 in RT[0], kk + 3 in RT[1]
-            if (kk + 2 < nch) store_tile(kk + 2, RT[0], ubuf[0]);
-            load_tile(min(kk + 4, nch - 1), RT[0]);
-            if constexpr (MODE != kSegState) write_y(kk, ystage[0]);
-            lds_barrier();
+        for (int64_t kk = 0; kk < nfull; kk += PF) {
+#pragma unroll
+            for (int p = 0; p < PF; ++p) {
+                const int64_t c = kk + p;  // this phase's chunk
+                if (p > 0 && c >= nfull) break;
+                const int q = (p + 1) % PF;
+                compute_full(ubuf[p], ystage[p]);
+                if (c + 1 < nch) store_tile(c + 1, RT[q], ubuf[q]);
+                load_tile(min(c + 1 + PF, nch - 1), RT[q]);  // slot q is free again
+                if constexpr (MODE != kSegState)
+                    if (c > 0) write_y(c - 1, ystage[(p + PF - 1) % PF]);
+                lds_barrier();
+            }
         }
         if constexpr (MODE != kSegState)
-            if (nfull > 0) write_y(nfull - 1, ystage[(nfull - 1) % 2]);
+            if (nfull > 0) write_y(nfull - 1, ystage[(nfull - 1) % PF]);
     }
     if constexpr (MODE == kWhole) {
         if (nch > nfull) {  // chunk nfull (staged); segmented launches have none
