@@ -148,6 +148,11 @@ __global__ __launch_bounds__(kBlock) void step_pairs_kernel(
         uv[i] = io_load(u + row);
     }
     const float hz = h0[cc];
+    // a use of every u value here keeps all the loads above issued together:
+    // left alone, the compiler sinks the first row's u load into its
+    // conditional store block, where it is issued only after the first wait
+#pragma unroll
+    for (int i = 0; i < NB; ++i) asm volatile("" ::"v"(uv[i]));
 #pragma unroll
     for (int i = 0; i < NB; ++i) {
         const int b = b0 + i;
