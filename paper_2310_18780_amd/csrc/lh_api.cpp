@@ -238,7 +238,8 @@ lh_status lh_prefill(const lh_c32* lambda, const lh_c32* R, const float* h0, con
     if (!lh::make_prefill_plan(B, D, d, T, chunk_len, io_dtype == LH_BF16 ? 1 : 0, &plan))
         return fail(LH_ERR_INVALID_ARG, "no prefill plan for these sizes%s",
                     chunk_len == LH_PREFILL_MFMA
-                        ? " (the matrix-core plan needs d = 16 or 32, D % 8 == 0, T >= 1)"
+                        ? " (the matrix-core plan needs T >= 1 and d = 16 or 32 with D % 8 == 0, "
+                          "or d = 64 with float32 u/y and D % 4 == 0)"
                     : chunk_len == LH_PREFILL_MFMA_SEG
                         ? " (the segmented matrix-core plan also needs T = s * 2^k * 32 "
                           "steps, k >= 1, segments of at least 256 steps)"

@@ -63,14 +63,20 @@ hipError_t launch_prefill(const float2* lam, const float2* R, const float* h0,
                           int64_t T, float2* state, void* y, const PrefillPlan& plan,
                           void* workspace, hipStream_t stream);
 
-// Matrix-core prefill (d = 16 or 32, D a multiple of 8).
-bool mfma_supported(int64_t B, int64_t D, int64_t d, int64_t T);
-// Whether the automatic plan takes the whole-prompt matrix-core plan.
+// Matrix-core prefill: d = 16 or 32 with D a multiple of 8 (bfloat16
+// operands), or d = 64 with float32 u/y and D a multiple of 4 (float32
+// operands).
+bool mfma_supported(int64_t B, int64_t D, int64_t d, int64_t T, bool bf16_io);
+// Whether the automatic plan takes the whole-prompt matrix-core plan over the
+// segmented one.
 bool mfma_preferred(int64_t B, int64_t D, int64_t d, int64_t T, bool bf16_io);
+// The automatic plan where the matrix-core plans are supported: 0 the VALU
+// scan, 1 the whole-prompt matrix-core plan, 2 the segmented one.
+int mfma_auto_plan(int64_t B, int64_t D, int64_t d, int64_t T, bool bf16_io);
 size_t mfma_workspace_bytes(int64_t D, int64_t d);
 // Segment count of the segmented matrix-core plan (0 when T does not split
 // into segments of a multiple of 32 steps, at least 256 long).
-int64_t mfma_segments(int64_t B, int64_t D, int64_t T);
+int64_t mfma_segments(int64_t B, int64_t D, int64_t d, int64_t T);
 hipError_t launch_mfma_setup(const float2* lam, const float2* R, const float* h0, int64_t D,
                              int64_t d, void* workspace, hipStream_t stream);
 // One pass of the segmented plan: outputs = false writes each segment's end

@@ -291,11 +291,14 @@ bool make_prefill_plan(int64_t B, int64_t D, int64_t d, int64_t T, int64_t chunk
                        PrefillPlan* plan)
 {
     if (io < 0) {  // workspace for either input type
-        PrefillPlan pb;
-        if (!make_prefill_plan(B, D, d, T, chunk_len, 0, plan) ||
-            !make_prefill_plan(B, D, d, T, chunk_len, 1, &pb))
-            return false;
-        if (pb.ws_bytes > plan->ws_bytes) plan->ws_bytes = pb.ws_bytes;
+        // (a type with no plan for these sizes, such as bfloat16 under the
+        // forced matrix-core plan at d = 64, adds nothing)
+        PrefillPlan pf, pb;
+        const bool f = make_prefill_plan(B, D, d, T, chunk_len, 0, &pf);
+        const bool b = make_prefill_plan(B, D, d, T, chunk_len, 1, &pb);
+        if (!f && !b) return false;
+        *plan = f ? pf : pb;
+        if (f && b && pb.ws_bytes > plan->ws_bytes) plan->ws_bytes = pb.ws_bytes;
         return true;
     }
     if (B < 1 || D < 1 || d < 1 || d > 1024 || T < 0 || chunk_len < -2) return false;
@@ -349,19 +352,21 @@ bool make_prefill_plan(int64_t B, int64_t D, int64_t d, int64_t T, int64_t chunk
     // workspace also covers the VALU plan above, taken when u or y is not
     // 16-byte aligned.
     p.mfma_forced = chunk_len == -1 || chunk_len == -2;
-    if (p.mfma_forced && !mfma_supported(B, D, d, T)) return false;
-    p.mfma = chunk_len == -1 ||
-             (chunk_len == 0 && mfma_supported(B, D, d, T) && mfma_preferred(B, D, d, T, io == 1));
+    if (p.mfma_forced && !mfma_supported(B, D, d, T, io == 1)) return false;
+    const int choice = chunk_len == 0 && mfma_supported(B, D, d, T, io == 1)
+                           ? mfma_auto_plan(B, D, d, T, io == 1)
+                           : 0;
+    p.mfma = chunk_len == -1 || choice == 1;
     p.mfma_seg = false;
     p.off_mfma = 0;
     if (p.mfma) {
         const size_t mb = mfma_workspace_bytes(D, d);
         if (p.mfma_forced || mb > p.ws_bytes) p.ws_bytes = mb;  // a forced plan has no fallback
-    } else if ((chunk_len == 0 || chunk_len == -2) && mfma_supported(B, D, d, T)) {
+    } else if (chunk_len == -2 || choice == 2) {
         // too few (batch row, channel group) tiles for the whole-prompt matrix-core
         // plan: cut the prompt into segments that run in parallel, on the matrix
         // cores, with the chunked scan's carry in between
-        const int64_t nseg = mfma_segments(B, D, T);
+        const int64_t nseg = mfma_segments(B, D, d, T);
         if (nseg >= 2) {
             p.mfma_seg = true;
             p.C = T / nseg;

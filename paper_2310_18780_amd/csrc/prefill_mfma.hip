@@ -71,6 +71,19 @@ constexpr int kMinWorkgroups = 256;  // automatic plan: at least one workgroup p
 // A-operand fragments per channel: P (2d/16 tiles), T (2 tiles), W (2 tiles x d/16 K-steps)
 __host__ __device__ constexpr int n_frag(int DM) { return 2 * DM + 2 + 2 * DM; }
 
+// d = 64 (DM = 4) runs on v_mfma_f32_16x16x4_f32 instead: float32 operands,
+// one float per lane per 16 x 4 block (lane l holds A[l % 16][l / 16] and
+// B[l / 16][l % 16]), no splitting, K = 4 per instruction.  A-operand blocks
+// per channel: P 2 DM row tiles x 8 K-steps, T 2 x 8, W 2 x 2 DM x 4.  The
+// three-term bfloat16 operands of 64 modes would not fit the registers.
+__host__ __device__ constexpr int n_frag32(int DM) { return 16 * DM + 16 + 16 * DM; }
+
+size_t frag_bytes_of(int64_t D, int DM)
+{
+    return DM == 4 ? size_t(D) * n_frag32(DM) * 64 * sizeof(float)
+                   : size_t(D) * n_frag(DM) * kTerms * 64 * sizeof(bf16x8);
+}
+
 __device__ __forceinline__ void split3(float v, __bf16& a, __bf16& b, __bf16& c)
 {
     a = static_cast<__bf16>(v);
@@ -104,6 +117,11 @@ __device__ __forceinline__ f32x4 mfma(bf16x8 a, bf16x8 b, f32x4 c)
     return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
 }
 
+__device__ __forceinline__ f32x4 mfma32(float a, float b, f32x4 c)
+{
+    return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
+
 // Workgroup barrier that orders LDS only: waits for this wave's LDS accesses
 // (lgkmcnt(0); vmcnt and expcnt left at their maximum in the s_waitcnt
 // encoding) and leaves global loads in flight, unlike __syncthreads(), whose
@@ -131,7 +149,7 @@ __global__ __launch_bounds__(256) void mfma_setup_kernel(const float2* __restric
                                                          float2* __restrict__ lamc)
 {
     constexpr int d = 16 * DM;
-    constexpr int F = n_frag(DM);
+    constexpr int F = DM == 4 ? n_frag32(DM) : n_frag(DM);
     __shared__ double pwr[d][kC + 1], pwi[d][kC + 1];
     __shared__ double taps[kC];
     const int c = blockIdx.x;
@@ -171,6 +189,28 @@ __global__ __launch_bounds__(256) void mfma_setup_kernel(const float2* __restric
         }
         const int f = item / 64, lane = item % 64;
         const int g = lane / 16, m = lane % 16;
+        if constexpr (DM == 4) {  // float32 blocks; K-step s of a chunk takes steps 8 g + s
+            double val;
+            if (f < 16 * DM) {  // P row tile q, K-step s: row 16 q + m, step 8 g + s
+                const int q = f / 8, s2 = f % 8;
+                const int r = 16 * q + m, j = 8 * g + s2;
+                val = r < d ? pwr[r][kC - 1 - j] : pwi[r - d][kC - 1 - j];
+            } else if (f < 16 * DM + 16) {  // T row tile mt, K-step s
+                const int mt = (f - 16 * DM) / 8, s2 = (f - 16 * DM) % 8;
+                const int t = 16 * mt + m, j = 8 * g + s2;
+                val = j <= t ? taps[t - j] : 0.0;
+            } else {  // W row tile mt, state tile q (Re q < DM, else Im), row i of the lane's 4
+                const int w = f - 16 * DM - 16;
+                const int mt = w / (8 * DM), q = (w % (8 * DM)) / 4, i = w % 4;
+                const int t = 16 * mt + m;
+                const int n = 16 * (q % DM) + 4 * g + i;
+                const double rr = rc[n].x, ri = rc[n].y;
+                val = q < DM ? rr * pwr[n][t] - ri * pwi[n][t]      // Re(R lambda^t)
+                             : -(rr * pwi[n][t] + ri * pwr[n][t]);  // -Im(R lambda^t)
+            }
+            reinterpret_cast<float*>(frag)[(int64_t(c) * F + f) * 64 + lane] = float(val);
+            continue;
+        }
         bf16x8 t0, t1, t2;
         for (int i = 0; i < 8; ++i) {
             const int k = 8 * g + i;  // K index of this element
@@ -231,8 +271,14 @@ template <>
 struct Tiling<float, 2> {
     static constexpr int CPW = 1;
 };
-constexpr int kW = 8;  // waves per workgroup
-constexpr int kThreads = 64 * kW;
+template <>
+struct Tiling<float, 4> {
+    static constexpr int CPW = 1;
+};
+// Waves per workgroup: 8 (two per SIMD) with bfloat16 operands; 4 with the
+// float32 operands of d = 64, whose 144 A values per lane and channel need
+// the whole register file of a SIMD (one wave each, up to 512 registers).
+__host__ __device__ constexpr int waves_of(int DM) { return DM == 4 ? 4 : 8; }
 
 // LDS element type of the staged u tile and operand term counts: bfloat16
 // inputs are exact in one term and their outputs are rounded to bfloat16, so
@@ -270,7 +316,7 @@ enum { kWhole = 0, kSegState = 1, kSegOut = 2 };
 template <typename IO, int DM, int MODE>
 constexpr int cpw_of()
 {
-    return MODE == kSegState ? (sizeof(IO) == 2 && DM == 1 ? 4 : 2) : Tiling<IO, DM>::CPW;
+    return MODE == kSegState && DM < 4 ? (sizeof(IO) == 2 && DM == 1 ? 4 : 2) : Tiling<IO, DM>::CPW;
 }
 
 // Chunk tiles of u in flight while a chunk is computed (in registers, one
@@ -282,20 +328,25 @@ constexpr int cpw_of()
 template <typename IO, int DM, int MODE>
 constexpr int pf_of()
 {
-    return MODE == kSegState || (sizeof(IO) == 4 && DM == 2 && MODE == kWhole) ? 1 : 2;
+    return MODE == kSegState || DM == 4 || (sizeof(IO) == 4 && DM == 2 && MODE == kWhole) ? 1 : 2;
 }
 
 template <typename IO, int DM, int NBG, int MODE>
-__global__ __launch_bounds__(kThreads) void mfma_prefill_kernel(
+__global__ __launch_bounds__(64 * waves_of(DM)) void mfma_prefill_kernel(
     const float2* __restrict__ lam, const IO* __restrict__ u, IO* __restrict__ y,
     float2* __restrict__ state, const bf16x8* __restrict__ frag,
     const float2* __restrict__ lamc, int B, int D, int64_t T, int ncg, int nbg, int per_xcd,
     int nseg, int64_t seg_len, float2* __restrict__ xs)
 {
     constexpr int d = 16 * DM;
-    constexpr int F = n_frag(DM);
+    constexpr bool k32 = DM == 4;                     // float32 operands (v_mfma_f32_16x16x4_f32)
+    static_assert(!k32 || sizeof(IO) == 4, "d = 64 takes float32 u and y");
+    constexpr int F = k32 ? 1 : n_frag(DM);
+    constexpr int F32 = k32 ? n_frag32(DM) : 1;
     constexpr int CPW = cpw_of<IO, DM, MODE>();
-    constexpr int CW = kW * CPW;
+    constexpr int NW = waves_of(DM);
+    constexpr int NT = 64 * NW;                       // threads
+    constexpr int CW = NW * CPW;
     constexpr int BN = kN * NBG;                      // batch rows per workgroup
     constexpr int NTU = Stage<IO>::kNTU;
     constexpr int KT = Stage<IO>::kNTA;
@@ -304,7 +355,7 @@ __global__ __launch_bounds__(kThreads) void mfma_prefill_kernel(
     constexpr int CPP = 16 / ES;                      // channels per 16-byte piece
     constexpr int PPR = CW / CPP;                     // pieces per (row, step)
     constexpr int NITEM = BN * (kC / 2) * PPR;        // (row, step pair, piece) items
-    constexpr int IPT = (NITEM + kThreads - 1) / kThreads;  // items per thread
+    constexpr int IPT = (NITEM + NT - 1) / NT;  // items per thread
     constexpr int US = kC + 16 / int(sizeof(ST));     // u stage: steps per (channel, row), padded
     // y stage in 32-bit words: (row, step) cells of SD words, rows padded to
     // 4 words past a multiple of 32 and the words of each 16-byte piece
@@ -346,14 +397,21 @@ __global__ __launch_bounds__(kThreads) void mfma_prefill_kernel(
     // ---- A operands and lambda^C of this wave's channels (clamped into range;
     // results of channels >= D are never stored)
     bf16x8 A[CPW][F][KT];
+    float A32[CPW][F32];
 #pragma unroll
     for (int k = 0; k < CPW; ++k) {
         const int cc = min(c0 + w * CPW + k, D - 1);
+        if constexpr (k32) {
+            const float* fr = reinterpret_cast<const float*>(frag) + int64_t(cc) * F32 * 64 + lane;
 #pragma unroll
-        for (int f = 0; f < F; ++f)
+            for (int f = 0; f < F32; ++f) A32[k][f] = fr[f * 64];
+        } else {
 #pragma unroll
-            for (int s = 0; s < KT; ++s)
-                A[k][f][s] = frag[((int64_t(cc) * F + f) * kTerms + s) * 64 + lane];
+            for (int f = 0; f < F; ++f)
+#pragma unroll
+                for (int s = 0; s < KT; ++s)
+                    A[k][f][s] = frag[((int64_t(cc) * F + f) * kTerms + s) * 64 + lane];
+        }
         if (n < 4 * DM)  // lambda^C of the modes of lane group g (read back by the carry)
             lcs[w * CPW + k][g][n] = lamc[(int64_t(cc) * 4 + g) * (4 * DM) + n];
     }
@@ -385,13 +443,13 @@ __global__ __launch_bounds__(kThreads) void mfma_prefill_kernel(
 
     const int64_t nch = (TL + kC - 1) / kC;
 
-    // ---- u staging: item p = tid + j kThreads holds (row p / (16 PPR), steps
+    // ---- u staging: item p = tid + j NT holds (row p / (16 PPR), steps
     // 2 ((p / PPR) % 16) + {0, 1}, channels c0 + CPP (p % PPR) ..).  Loads are
     // unconditional, from addresses clamped into the tensor, so that no
     // control flow surrounds the destination registers; rows, steps and
     // channels outside the tensor are zeroed when the tile is staged.
     auto item_of = [&](int j, int& ip, int& itp, int& irb) {
-        const int p = min(tid + j * kThreads, NITEM - 1);
+        const int p = min(tid + j * NT, NITEM - 1);
         ip = p % PPR;
         itp = (p / PPR) % (kC / 2);
         irb = p / (PPR * (kC / 2));
@@ -431,7 +489,7 @@ __global__ __launch_bounds__(kThreads) void mfma_prefill_kernel(
     auto store_tile = [&](int64_t kk, const auto& R0, ST* ub) {
 #pragma unroll
         for (int j = 0; j < IPT; ++j) {
-            if (tid + j * kThreads >= NITEM) continue;
+            if (tid + j * NT >= NITEM) continue;
             int ip, itp, irb;
             item_of(j, ip, itp, irb);
             const bool in = b0 + irb < BV && c0 + ip * CPP < D;
@@ -472,6 +530,51 @@ __global__ __launch_bounds__(kThreads) void mfma_prefill_kernel(
                 U[0][i] = a;
                 U[1][i] = b2;
                 U[2][i] = c2;
+            }
+        }
+    };
+    // the same steps as float32 B operands, one per K-step of 16x16x4
+    auto load_u32 = [&](int k, int bg, float (&U)[8], const ST* ub) {
+        const int ue = ((w * CPW + k) * BN + kN * bg + n) * US + 8 * g;
+        const float4 lo = *reinterpret_cast<const float4*>(&ub[ue]);
+        const float4 hi = *reinterpret_cast<const float4*>(&ub[ue + 4]);
+        U[0] = lo.x, U[1] = lo.y, U[2] = lo.z, U[3] = lo.w;
+        U[4] = hi.x, U[5] = hi.y, U[6] = hi.z, U[7] = hi.w;
+    };
+    // float32 operands (d = 64), one channel k and batch group bg: outputs of
+    // the chunk from the entry state, Y = T U + W X_in (K-step (q, i) of W X_in
+    // takes row i of state tile q, which each lane already holds)
+    auto y32 = [&](int k, const float (&U)[8], const f32x4 (&Xs)[2 * DM], f32x4 (&Y)[2]) {
+        Y[0] = Y[1] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int s = 0; s < 8; ++s)
+#pragma unroll
+            for (int mt = 0; mt < 2; ++mt) Y[mt] = mfma32(A32[k][16 * DM + 8 * mt + s], U[s], Y[mt]);
+#pragma unroll
+        for (int q = 0; q < 2 * DM; ++q)
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int mt = 0; mt < 2; ++mt)
+                    Y[mt] = mfma32(A32[k][16 * DM + 16 + 8 * DM * mt + 4 * q + i], Xs[q][i], Y[mt]);
+    };
+    // chunk end state from the chunk's inputs, S = P U, and the carry
+    // X <- lambda^C X + S, one state tile pair (Re q, Im q) at a time
+    auto carry32 = [&](int k, int bg, const float (&U)[8]) {
+#pragma unroll
+        for (int q = 0; q < DM; ++q) {
+            f32x4 Sr = f32x4{0.f, 0.f, 0.f, 0.f}, Si = Sr;
+#pragma unroll
+            for (int s = 0; s < 8; ++s) {
+                Sr = mfma32(A32[k][8 * q + s], U[s], Sr);
+                Si = mfma32(A32[k][8 * (DM + q) + s], U[s], Si);
+            }
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const float2 l = lcs[w * CPW + k][g][4 * q + i];
+                const float xr = X[k][bg][q][i], xi = X[k][bg][DM + q][i];
+                X[k][bg][q][i] = fmaf(l.x, xr, fmaf(-l.y, xi, Sr[i]));
+                X[k][bg][DM + q][i] = fmaf(l.x, xi, fmaf(l.y, xr, Si[i]));
             }
         }
     };
@@ -521,62 +624,77 @@ __global__ __launch_bounds__(kThreads) void mfma_prefill_kernel(
     // for all independent accumulators of the wave's channels (2 Y tiles and
     // 2 DM S tiles per channel), then the carry and the output stage
     auto compute_full = [&](const ST* ub, uint32_t* ys) {
+        if constexpr (k32) {
 #pragma unroll
-        for (int bg = 0; bg < NBG; ++bg) {
-            bf16x8 U[CPW][NTU];
-            bf16x8 XB[CPW][DM][2];
-            f32x4 Y[CPW][2], Sr[CPW][DM], Si[CPW][DM];
+            for (int bg = 0; bg < NBG; ++bg) {
+                f32x4 Y[CPW][2];
 #pragma unroll
-            for (int k = 0; k < CPW; ++k) {
-                load_u(k, bg, U[k], ub);
-                if constexpr (MODE != kSegState) split_x(X[k][bg], XB[k]);
-                Y[k][0] = Y[k][1] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-                for (int q = 0; q < DM; ++q) Sr[k][q] = Si[k][q] = f32x4{0.f, 0.f, 0.f, 0.f};
+                for (int k = 0; k < CPW; ++k) {
+                    float U[8];
+                    load_u32(k, bg, U, ub);
+                    if constexpr (MODE != kSegState) y32(k, U, X[k][bg], Y[k]);
+                    carry32(k, bg, U);
+                }
+                if constexpr (MODE != kSegState) stage_y(bg, Y, ys);
             }
+        } else {
 #pragma unroll
-            for (int ia = 0; ia < KT; ++ia)
+            for (int bg = 0; bg < NBG; ++bg) {
+                bf16x8 U[CPW][NTU];
+                bf16x8 XB[CPW][DM][2];
+                f32x4 Y[CPW][2], Sr[CPW][DM], Si[CPW][DM];
 #pragma unroll
-                for (int ju = 0; ju < NTU; ++ju) {
-                    if (ia + ju >= KT) continue;
+                for (int k = 0; k < CPW; ++k) {
+                    load_u(k, bg, U[k], ub);
+                    if constexpr (MODE != kSegState) split_x(X[k][bg], XB[k]);
+                    Y[k][0] = Y[k][1] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-                    for (int k = 0; k < CPW; ++k) {
-                        if constexpr (MODE != kSegState) {
+                    for (int q = 0; q < DM; ++q) Sr[k][q] = Si[k][q] = f32x4{0.f, 0.f, 0.f, 0.f};
+                }
 #pragma unroll
-                            for (int mt = 0; mt < 2; ++mt)
-                                Y[k][mt] = mfma(A[k][2 * DM + mt][ia], U[k][ju], Y[k][mt]);
-                        }
+                for (int ia = 0; ia < KT; ++ia)
 #pragma unroll
-                        for (int q = 0; q < DM; ++q) {
-                            Sr[k][q] = mfma(A[k][q][ia], U[k][ju], Sr[k][q]);
-                            Si[k][q] = mfma(A[k][DM + q][ia], U[k][ju], Si[k][q]);
+                    for (int ju = 0; ju < NTU; ++ju) {
+                        if (ia + ju >= KT) continue;
+#pragma unroll
+                        for (int k = 0; k < CPW; ++k) {
+                            if constexpr (MODE != kSegState) {
+#pragma unroll
+                                for (int mt = 0; mt < 2; ++mt)
+                                    Y[k][mt] = mfma(A[k][2 * DM + mt][ia], U[k][ju], Y[k][mt]);
+                            }
+#pragma unroll
+                            for (int q = 0; q < DM; ++q) {
+                                Sr[k][q] = mfma(A[k][q][ia], U[k][ju], Sr[k][q]);
+                                Si[k][q] = mfma(A[k][DM + q][ia], U[k][ju], Si[k][q]);
+                            }
                         }
                     }
-                }
-            if constexpr (MODE != kSegState) {
+                if constexpr (MODE != kSegState) {
 #pragma unroll
-                for (int p = 0; p < kWX; ++p)
+                    for (int p = 0; p < kWX; ++p)
+#pragma unroll
+                        for (int q = 0; q < DM; ++q)
+#pragma unroll
+                            for (int k = 0; k < CPW; ++k)
+#pragma unroll
+                                for (int mt = 0; mt < 2; ++mt)
+                                    Y[k][mt] = mfma(A[k][2 * DM + 2 + mt * DM + q][kWXa[p]],
+                                                    XB[k][q][kWXx[p]], Y[k][mt]);
+                }
+#pragma unroll
+                for (int k = 0; k < CPW; ++k)
 #pragma unroll
                     for (int q = 0; q < DM; ++q)
 #pragma unroll
-                        for (int k = 0; k < CPW; ++k)
-#pragma unroll
-                            for (int mt = 0; mt < 2; ++mt)
-                                Y[k][mt] = mfma(A[k][2 * DM + 2 + mt * DM + q][kWXa[p]],
-                                                XB[k][q][kWXx[p]], Y[k][mt]);
+                        for (int i = 0; i < 4; ++i) {  // carry: X <- lambda^C X + S
+                            const float2 l = lcs[w * CPW + k][g][4 * q + i];
+                            const float xr = X[k][bg][q][i], xi = X[k][bg][DM + q][i];
+                            X[k][bg][q][i] = fmaf(l.x, xr, fmaf(-l.y, xi, Sr[k][q][i]));
+                            X[k][bg][DM + q][i] = fmaf(l.x, xi, fmaf(l.y, xr, Si[k][q][i]));
+                        }
+                if constexpr (MODE != kSegState) stage_y(bg, Y, ys);
             }
-#pragma unroll
-            for (int k = 0; k < CPW; ++k)
-#pragma unroll
-                for (int q = 0; q < DM; ++q)
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) {  // carry: X <- lambda^C X + S
-                        const float2 l = lcs[w * CPW + k][g][4 * q + i];
-                        const float xr = X[k][bg][q][i], xi = X[k][bg][DM + q][i];
-                        X[k][bg][q][i] = fmaf(l.x, xr, fmaf(-l.y, xi, Sr[k][q][i]));
-                        X[k][bg][DM + q][i] = fmaf(l.x, xi, fmaf(l.y, xr, Si[k][q][i]));
-                    }
-            if constexpr (MODE != kSegState) stage_y(bg, Y, ys);
         }
     };
 
@@ -588,24 +706,30 @@ __global__ __launch_bounds__(kThreads) void mfma_prefill_kernel(
             f32x4 Y[CPW][2];
 #pragma unroll
             for (int k = 0; k < CPW; ++k) {
-                bf16x8 U[NTU];
-                bf16x8 XB[DM][2];
-                load_u(k, bg, U, ub);
-                split_x(X[k][bg], XB);
+                if constexpr (k32) {
+                    float U[8];
+                    load_u32(k, bg, U, ub);
+                    y32(k, U, X[k][bg], Y[k]);
+                } else {
+                    bf16x8 U[NTU];
+                    bf16x8 XB[DM][2];
+                    load_u(k, bg, U, ub);
+                    split_x(X[k][bg], XB);
 #pragma unroll
-                for (int mt = 0; mt < 2; ++mt) {
-                    Y[k][mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+                    for (int mt = 0; mt < 2; ++mt) {
+                        Y[k][mt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-                    for (int ia = 0; ia < KT; ++ia)
+                        for (int ia = 0; ia < KT; ++ia)
 #pragma unroll
-                        for (int ju = 0; ju < NTU; ++ju)
-                            if (ia + ju < KT) Y[k][mt] = mfma(A[k][2 * DM + mt][ia], U[ju], Y[k][mt]);
+                            for (int ju = 0; ju < NTU; ++ju)
+                                if (ia + ju < KT) Y[k][mt] = mfma(A[k][2 * DM + mt][ia], U[ju], Y[k][mt]);
 #pragma unroll
-                    for (int p = 0; p < kWX; ++p)
+                        for (int p = 0; p < kWX; ++p)
 #pragma unroll
-                        for (int q = 0; q < DM; ++q)
-                            Y[k][mt] = mfma(A[k][2 * DM + 2 + mt * DM + q][kWXa[p]],
-                                            XB[q][kWXx[p]], Y[k][mt]);
+                            for (int q = 0; q < DM; ++q)
+                                Y[k][mt] = mfma(A[k][2 * DM + 2 + mt * DM + q][kWXa[p]],
+                                                XB[q][kWXx[p]], Y[k][mt]);
+                    }
                 }
             }
             stage_y(bg, Y, ys);
@@ -640,8 +764,8 @@ __global__ __launch_bounds__(kThreads) void mfma_prefill_kernel(
     auto write_y = [&](int64_t kk, const uint32_t* ys) {
         const int64_t t0 = kk * kC;
 #pragma unroll
-        for (int j = 0; j < (NYP + kThreads - 1) / kThreads; ++j) {
-            const int r = tid + j * kThreads;
+        for (int j = 0; j < (NYP + NT - 1) / NT; ++j) {
+            const int r = tid + j * NT;
             const int rp = r % PPR, rt = (r / PPR) % kC, rb = r / (PPR * kC);
             const int64_t gt = t0 + rt;
             if (r < NYP && b0 + rb < BV && gt < TL && c0 + rp * CPP < D) {
@@ -746,10 +870,11 @@ __global__ __launch_bounds__(kThreads) void mfma_prefill_kernel(
 }
 
 // batch groups of 16 rows per wave: two when there are more than 16 rows and
-// the registers allow (float32 inputs with d = 16, one channel per wave)
+// the registers allow (float32 inputs with d = 16, one channel per wave; d =
+// 64, whose waves have a SIMD's registers to themselves)
 int mfma_nbg(int64_t B, int64_t d, bool bf16_io)
 {
-    return d == 16 && !bf16_io && B > kN ? 2 : 1;
+    return ((d == 16 && !bf16_io) || d == 64) && B > kN ? 2 : 1;
 }
 
 template <typename IO, int DM, int NBG, int MODE>
@@ -757,7 +882,7 @@ hipError_t launch_main(const float2* lam, const void* u, void* y, float2* state,
                        const bf16x8* frag, const float2* lamc, int64_t B, int64_t D, int64_t T,
                        int nseg, int64_t seg_len, float2* xs, hipStream_t stream)
 {
-    constexpr int CW = kW * cpw_of<IO, DM, MODE>();
+    constexpr int CW = waves_of(DM) * cpw_of<IO, DM, MODE>();
     const int64_t sv = MODE == kWhole ? 1 : MODE == kSegState ? nseg - 1 : nseg;
     const int64_t ncg = (D + CW - 1) / CW;
     const int64_t nbg = (B * sv + kN * NBG - 1) / (kN * NBG);
@@ -765,7 +890,7 @@ hipError_t launch_main(const float2* lam, const void* u, void* y, float2* state,
     const int64_t grid = 8 * per_xcd;
     if (grid > 0x7fffffff || B * sv > 0x7fffffff) return hipErrorInvalidConfiguration;
     hipLaunchKernelGGL((mfma_prefill_kernel<IO, DM, NBG, MODE>), dim3(uint32_t(grid)),
-                       dim3(kThreads), 0, stream, lam, static_cast<const IO*>(u),
+                       dim3(64 * waves_of(DM)), 0, stream, lam, static_cast<const IO*>(u),
                        static_cast<IO*>(y), state, frag, lamc, int(B), int(D), T, int(ncg),
                        int(nbg), int(per_xcd), nseg, seg_len, xs);
     return hipGetLastError();
@@ -777,13 +902,20 @@ hipError_t launch_mode(const float2* lam, const void* u, bool bf16_io, int64_t B
                        int nseg, int64_t seg_len, float2* xs, hipStream_t stream)
 {
     const int DM = int(d / 16);
-    const size_t frag_bytes = size_t(D) * n_frag(DM) * kTerms * 64 * sizeof(bf16x8);
+    const size_t frag_bytes = frag_bytes_of(D, DM);
     const bf16x8* frag = static_cast<const bf16x8*>(workspace);
     const float2* lamc = reinterpret_cast<const float2*>(static_cast<const char*>(workspace) +
                                                          (frag_bytes + 255) / 256 * 256);
     // rows of the MFMA columns: batch rows or (batch row, segment) pairs
     const int64_t rows = MODE == kWhole ? B : MODE == kSegState ? B * (nseg - 1) : B * nseg;
     const bool two = mfma_nbg(rows, d, bf16_io) == 2;
+    if (DM == 4) {  // float32 u/y only (mfma_supported)
+        if (bf16_io) return hipErrorInvalidValue;
+        return two ? launch_main<float, 4, 2, MODE>(lam, u, y, state, frag, lamc, B, D, T, nseg,
+                                                    seg_len, xs, stream)
+                   : launch_main<float, 4, 1, MODE>(lam, u, y, state, frag, lamc, B, D, T, nseg,
+                                                    seg_len, xs, stream);
+    }
     if (bf16_io)
         return DM == 2 ? launch_main<bf16, 2, 1, MODE>(lam, u, y, state, frag, lamc, B, D, T,
                                                        nseg, seg_len, xs, stream)
@@ -803,15 +935,15 @@ hipError_t launch_mode(const float2* lam, const void* u, bool bf16_io, int64_t B
 // Workspace of the MFMA plan: fragments then lambda^C.
 size_t mfma_workspace_bytes(int64_t D, int64_t d)
 {
-    const int DM = int(d / 16);
-    const size_t frag = size_t(D) * n_frag(DM) * kTerms * 64 * sizeof(bf16x8);
+    const size_t frag = frag_bytes_of(D, int(d / 16));
     const size_t lamc = size_t(D) * d * sizeof(float2);
     return (frag + 255) / 256 * 256 + lamc;
 }
 
-bool mfma_supported(int64_t B, int64_t D, int64_t d, int64_t T)
+bool mfma_supported(int64_t B, int64_t D, int64_t d, int64_t T, bool bf16_io)
 {
-    return (d == 16 || d == 32) && D % kW == 0 && T >= 1 && B <= (INT64_C(1) << 30) &&
+    const bool tiles = d == 16 || d == 32 ? D % 8 == 0 : d == 64 && !bf16_io && D % 4 == 0;
+    return tiles && T >= 1 && B <= (INT64_C(1) << 30) &&
            D <= (INT64_C(1) << 30);
 }
 
@@ -819,13 +951,14 @@ bool mfma_supported(int64_t B, int64_t D, int64_t d, int64_t T)
 // and at least 256 steps long) whose (batch row, segment) columns give at
 // least kSegWorkgroups workgroups of 8 channels, else the most segments
 // allowed.
-int64_t mfma_segments(int64_t B, int64_t D, int64_t T)
+int64_t mfma_segments(int64_t B, int64_t D, int64_t d, int64_t T)
 {
     constexpr int64_t kSegWorkgroups = 1024, kMinSeg = 256;
+    const int64_t cw = waves_of(int(d / 16));
     int64_t best = 0;
     for (int64_t s = 2; T % (s * kC) == 0 && T / s >= kMinSeg; s *= 2) {
         best = s;
-        if ((B * s + kN - 1) / kN * ((D + kW - 1) / kW) >= kSegWorkgroups) break;
+        if ((B * s + kN - 1) / kN * ((D + cw - 1) / cw) >= kSegWorkgroups) break;
     }
     return best;
 }
@@ -841,11 +974,11 @@ int64_t mfma_segments(int64_t B, int64_t D, int64_t T)
 template <int MODE>
 int64_t pass_slots(int64_t rows, int64_t D, int64_t d, bool bf16_io, int64_t chunks)
 {
-    const bool dm2 = d == 32;
-    const int cpw = bf16_io ? (dm2 ? cpw_of<bf16, 2, MODE>() : cpw_of<bf16, 1, MODE>())
-                            : (dm2 ? cpw_of<float, 2, MODE>() : cpw_of<float, 1, MODE>());
-    const int nbg = dm2 ? 1 : mfma_nbg(rows, d, bf16_io);
-    const int64_t cw = int64_t(kW) * cpw, bn = int64_t(kN) * nbg;
+    const int cpw = d == 64   ? 1
+                    : bf16_io ? (d == 32 ? cpw_of<bf16, 2, MODE>() : cpw_of<bf16, 1, MODE>())
+                              : (d == 32 ? cpw_of<float, 2, MODE>() : cpw_of<float, 1, MODE>());
+    const int nbg = mfma_nbg(rows, d, bf16_io);
+    const int64_t cw = int64_t(waves_of(int(d / 16))) * cpw, bn = int64_t(kN) * nbg;
     const int64_t wgs = (D + cw - 1) / cw * ((rows + bn - 1) / bn);
     return (wgs + kMinWorkgroups - 1) / kMinWorkgroups * chunks * nbg;
 }
@@ -859,7 +992,7 @@ bool mfma_preferred(int64_t B, int64_t D, int64_t d, int64_t T, bool bf16_io)
     // launches and second read of u, hence the 7/5 allowance, fitted to
     // measured times of both plans over B = 1..64, D = 768 / 2048, d = 16 /
     // 32, T = 1K..16K, float32 and bfloat16)
-    const int64_t nseg = mfma_segments(B, D, T);
+    const int64_t nseg = mfma_segments(B, D, d, T);
     if (nseg < 2) return false;
     const int64_t seg_chunks = T / nseg / kC;
     const int64_t whole = pass_slots<kWhole>(B, D, d, bf16_io, (T + kC - 1) / kC);
@@ -868,18 +1001,34 @@ bool mfma_preferred(int64_t B, int64_t D, int64_t d, int64_t T, bool bf16_io)
     return 5 * whole <= 7 * seg;
 }
 
+int mfma_auto_plan(int64_t B, int64_t D, int64_t d, int64_t T, bool bf16_io)
+{
+    // d = 64 with at most 1024 (row, step) pairs: the VALU plan's chunked scan
+    // beats both matrix-core plans (measured at D = 768 and 2048)
+    if (d == 64 && B * T <= 1024) return 0;
+    if (mfma_preferred(B, D, d, T, bf16_io)) return 1;
+    if (mfma_segments(B, D, d, T) >= 2) return 2;
+    // no segments: at d = 64 the whole prompt still beats the VALU plan once
+    // its workgroups (4 channels x 16 rows) fill the GPU
+    if (d == 64 && (D + 3) / 4 * ((B + kN - 1) / kN) >= kMinWorkgroups) return 1;
+    return 0;
+}
+
 hipError_t launch_mfma_setup(const float2* lam, const float2* R, const float* h0, int64_t D,
                              int64_t d, void* workspace, hipStream_t stream)
 {
     (void)hipGetLastError();
     const int DM = int(d / 16);
-    const size_t frag_bytes = size_t(D) * n_frag(DM) * kTerms * 64 * sizeof(bf16x8);
+    const size_t frag_bytes = frag_bytes_of(D, DM);
     bf16x8* frag = static_cast<bf16x8*>(workspace);
     float2* lamc = reinterpret_cast<float2*>(static_cast<char*>(workspace) +
                                              (frag_bytes + 255) / 256 * 256);
     if (D > 0x7fffffff) return hipErrorInvalidConfiguration;
     if (DM == 1)
         hipLaunchKernelGGL(mfma_setup_kernel<1>, dim3(uint32_t(D)), dim3(256), 0, stream, lam,
+                           R, h0, frag, lamc);
+    else if (DM == 4)
+        hipLaunchKernelGGL(mfma_setup_kernel<4>, dim3(uint32_t(D)), dim3(256), 0, stream, lam,
                            R, h0, frag, lamc);
     else
         hipLaunchKernelGGL(mfma_setup_kernel<2>, dim3(uint32_t(D)), dim3(256), 0, stream, lam,

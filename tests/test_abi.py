@@ -92,11 +92,18 @@ def test_workspace_sizes():
     assert lh.workspace_bytes(4, 1024, 32, 65536, chunk_len=2048) == 1024 * 32 * 8 + 4 * 32 * 1024 * 32 * 8
     # the segmented plan needs segments of >= 256 steps, a multiple of 32
     assert lh.lib().lh_prefill_workspace_bytes(4, 1024, 32, 500, -2) == ctypes.c_size_t(-1).value
-    # the matrix-core plan needs d = 16 / 32 and D % 8 == 0
+    # the matrix-core plan needs d = 16 / 32 and D % 8 == 0, or d = 64 and D % 4 == 0
     bad = ctypes.c_size_t(-1).value
     assert lh.lib().lh_prefill_workspace_bytes(2, 12, 16, 64, -1) == bad
-    assert lh.lib().lh_prefill_workspace_bytes(2, 16, 64, 64, -1) == bad
-    assert lh.workspace_bytes(256, 2048, 64, 1024) == 0
+    assert lh.lib().lh_prefill_workspace_bytes(2, 18, 64, 64, -1) == bad
+    assert lh.lib().lh_prefill_workspace_bytes(2, 8, 48, 64, -1) == bad
+    # d = 64: float32 blocks of P, T, W (64 + 16 + 64 blocks of 64 lanes x 4 B per
+    # channel), then lambda^C
+    assert lh.workspace_bytes(2, 12, 64, 64, chunk_len=-1) == up(12 * 144 * 64 * 4) + 12 * 64 * 8
+    # the wide d = 64 workload: the matrix-core plan with float32 blocks; with
+    # bfloat16 u/y (no matrix-core plan at d = 64) one VALU pass
+    assert lh.workspace_bytes(256, 2048, 64, 1024) == up(2048 * 144 * 64 * 4) + 2048 * 64 * 8
+    assert lh.prefill_plan(256, 2048, 64, 1024, io="bf16") == "scan"
     # D % 8 != 0: VALU plan, few rows -> 5 chunks of 64 steps
     assert lh.workspace_bytes(2, 70, 16, 300) == 70 * 16 * 8 + 2 * 5 * 70 * 16 * 8
     # invalid sizes
@@ -112,7 +119,12 @@ def test_prefill_plan_query():
     """lh_prefill_plan: the plan lh_prefill takes (host only, no device)."""
     P = lh.prefill_plan
     assert P(1, 4, 4, 64) == "scan"                    # d = 4: no matrix-core plan
-    assert P(256, 2048, 64, 1024) == "scan"            # d = 64
+    assert P(256, 2048, 64, 1024) == "mfma"            # d = 64: float32 matrix-core plan
+    assert P(256, 2048, 64, 1024, io="bf16") == "scan"  # d = 64 needs float32 u/y
+    assert P(1, 768, 64, 1024) == "scan"               # d = 64, B T <= 1024
+    assert P(4, 768, 64, 1024) == "mfma_seg"           # d = 64, few rows
+    assert P(16, 768, 64, 1000) == "scan"              # no segments, 192 workgroups
+    assert P(64, 768, 64, 1000) == "mfma"              # no segments, 768 workgroups
     assert P(64, 2048, 16, 4096, io="bf16") == "mfma"  # enough (channel, row) tiles
     assert P(4, 1024, 32, 65536) == "mfma_seg"         # 4 rows, long prompt
     assert P(16, 768, 16, 2048) == "mfma"              # chunk-step estimate: whole prompt
@@ -123,8 +135,9 @@ def test_prefill_plan_query():
     assert P(4, 1024, 32, 65536, chunk_len=2048) == "scan"
     assert P(2, 16, 16, 64, chunk_len=-1) == "mfma"
     assert P(2, 16, 16, 1024, chunk_len=-2) == "mfma_seg"
+    assert P(2, 12, 64, 64, chunk_len=-1) == "mfma"    # d = 64, float32 u/y
     L = lh.lib()
-    for args in [(2, 12, 16, 64, -1, 0), (4, 1024, 32, 500, -2, 0), (0, 1, 1, 1, 0, 0),
+    for args in [(2, 12, 16, 64, -1, 0), (2, 12, 64, 64, -1, 1), (2, 18, 64, 64, -1, 0), (4, 1024, 32, 500, -2, 0), (0, 1, 1, 1, 0, 0),
                  (1, 1, 1, 1, -3, 0), (1, 1, 1, 1, 0, 2), (1, 1, 1, -1, 0, 1)]:
         assert L.lh_prefill_plan(*args) == -1, args
 

@@ -101,6 +101,13 @@ SMALL = [
     (40, 16, 16, 1024, 3, "f32", -2),  # 2 column groups per wave (float32, d = 16)
     (2, 24, 16, 576, 3, "bf16", -2),   # two segments of 9 chunks (odd count), bfloat16
     (2, 24, 32, 576, 3, "f32", -2),    # the same with float32, d = 32
+    # d = 64: float32 operands, 4 channels per workgroup
+    (2, 12, 64, 96, 3, "f32", -1),     # three channel groups, three full chunks
+    (20, 8, 64, 70, 3, "f32", -1),     # second batch group of 4 rows; 70 = 2*32 + 6
+    (1, 4, 64, 20, 2, "f32", -1),      # only a partial chunk
+    (3, 4, 64, 1, 2, "f32", -1),       # T = 1
+    (2, 12, 64, 512, 3, "f32", -2),    # two segments of 256 steps
+    (3, 4, 64, 1024, 2, "f32", -2),    # four segments
 ]
 
 
@@ -341,6 +348,8 @@ def test_unaligned_io_falls_back_to_the_vector_scan(io):
     (2, 512, 32, 8192, "f32", -2),   # few rows, long prompt: the segmented plan
     (2, 512, 16, 8192, "bf16", -2),
     (64, 2048, 16, 256, "bf16", -1),
+    (4, 768, 64, 1024, "f32", -2),   # d = 64, few rows: segments
+    (32, 768, 64, 1000, "f32", -1),  # d = 64, no segments, 384 workgroups: whole prompt
 ])
 def test_automatic_plan_choice(case):
     """The automatic plan's outputs and state equal, bit for bit, those of the
