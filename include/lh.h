@@ -139,17 +139,23 @@ int lh_prefill_plan(int64_t B, int64_t D, int64_t d, int64_t T, int64_t chunk_le
  *                   ceil(T/chunk_len) chunks processed in parallel; chunk_len
  *                   >= T means one sequential pass per row);
  *                   LH_PREFILL_MFMA = the matrix-core plan (chunks of 32
- *                   steps as dense contractions on the MFMA units, float32
- *                   operands split into bfloat16 terms: three with float32
- *                   u/y, two with bfloat16 u/y; requires d = 16 or 32,
- *                   D % 8 == 0, T >= 1 and 16-byte aligned u and y, else
- *                   LH_ERR_INVALID_ARG).  The automatic plan uses it where
- *                   supported and either ceil(D/16) * ceil(B/32) >= 256
- *                   (enough workgroups to fill the GPU without splitting the
- *                   prompt in time) or an estimate of the chunk steps each
- *                   compute unit walks puts it within 7/5 of the segmented
- *                   plan below (the estimate depends on the input type, so
- *                   float32 and bfloat16 calls may take different plans);
+ *                   steps as dense contractions on the MFMA units; with d =
+ *                   16 or 32 the float32 operands are split into bfloat16
+ *                   terms, three with float32 u/y, two with bfloat16 u/y,
+ *                   and D % 8 == 0 is required; with d = 64 the operands
+ *                   stay float32 (16x16x4 float32 products), u/y must be
+ *                   float32 and D % 4 == 0; always T >= 1 and 16-byte
+ *                   aligned u and y, else LH_ERR_INVALID_ARG).  The
+ *                   automatic plan uses it where supported and either
+ *                   ceil(D/16) * ceil(B/32) >= 256 (enough workgroups to
+ *                   fill the GPU without splitting the prompt in time) or
+ *                   an estimate of the chunk steps each compute unit walks
+ *                   puts it within 7/5 of the segmented plan below (the
+ *                   estimate depends on the input type, so float32 and
+ *                   bfloat16 calls may take different plans); at d = 64
+ *                   also when T does not split into segments and
+ *                   ceil(D/4) * ceil(B/16) >= 256, and never when
+ *                   B * T <= 1024 (the VALU scan is faster there);
  *                   LH_PREFILL_MFMA_SEG = the segmented matrix-core plan: the
  *                   prompt is cut into 2^k segments of T / 2^k steps (a
  *                   multiple of 32, at least 256), the fewest whose (batch
@@ -160,7 +166,7 @@ int lh_prefill_plan(int64_t B, int64_t D, int64_t d, int64_t T, int64_t chunk_le
  *                   splitting and requirements as LH_PREFILL_MFMA, and such a
  *                   T).  The automatic plan takes it where the whole-prompt
  *                   matrix-core plan is supported but not chosen and T splits
- *                   this way
+ *                   this way (at d = 64 only when B * T > 1024)
  *   workspace     : device scratch of at least
  *                   lh_prefill_workspace_bytes(B,D,d,T,chunk_len) bytes,
  *                   256-byte aligned; may be NULL when that size is 0.  Its

@@ -33,15 +33,23 @@
 // split by the setup kernel into the workspace, already in the lane order of
 // the A operand.
 //
+// d = 64 (float32 u/y only) runs on v_mfma_f32_16x16x4_f32 without splitting:
+// the same three contractions as 144 products of K = 4 per channel, chunk and
+// 16 rows (64 for S, 16 for T U, 64 for W X_in), in float32 throughout.  Its
+// 144 operand values per lane and channel fill most of a SIMD's 512
+// registers, so its workgroups have 4 waves (one per SIMD, 4 channels) and
+// each wave takes two groups of 16 rows.
+//
 // Work layout: a wavefront owns CPW channels (2 for bfloat16 inputs with
-// d = 16, else 1) and NBG groups of 16 batch rows, and walks all chunks of the
+// d = 16, else 1) and NBG groups of 16 batch rows (2 for float32 inputs with
+// d = 16 or 64 and more than 16 rows, else 1), and walks all chunks of the
 // prompt, keeping its matrices (A operands) and the carried states in
 // registers.  With the 16x16 accumulator layout (lane n + 16 g holds rows
 // 4g..4g+3 of column n) and state rows ordered [Re modes | Im modes], the
 // real and imaginary parts of a mode sit in the same lane, so the carry is
 // lane-local, and X_in itself is the B operand of W X_in once W's columns are
 // permuted to match (K index 8g + i <-> the lane's rows).  A workgroup is 8
-// waves = 8 CPW consecutive channels.  The u tile of a chunk is staged
+// waves = 8 CPW consecutive channels (4 waves and channels at d = 64).  The u tile of a chunk is staged
 // through LDS (transposed to [channel][row][step]) from registers loaded one
 // or two chunks ahead (pf_of); the outputs go back through LDS so that every
 // global access is a 16-byte piece of a whole (row, step) segment of the
