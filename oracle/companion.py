@@ -36,7 +36,7 @@ from typing import Tuple
 
 import numpy as np
 
-__all__ = ["from_modal", "companion_run", "inverse_denominator_response", "fast_init"]
+__all__ = ["from_modal", "companion_matrix", "companion_run", "inverse_denominator_response", "fast_init"]
 
 
 def _pair_poles(lam, R):
@@ -69,20 +69,33 @@ def from_modal(lam, R, h0) -> Tuple[np.ndarray, np.ndarray, np.ndarray]:
     return a, beta, np.asarray(h0, np.float64).reshape(D).copy()
 
 
-def companion_run(a, beta, b0, u, x0=None) -> Tuple[np.ndarray, np.ndarray]:
-    """Step the companion recurrence of one channel over ``u [L]`` from ``x0``
-    (zeros by default).  Returns ``y [L]`` and the final state ``[2d]``."""
+def companion_matrix(a) -> np.ndarray:
+    """The ``2d x 2d`` state matrix of the companion canonical form
+    (eq. "ssm_canon"): first row ``-a``, ones on the subdiagonal."""
     a = np.asarray(a, np.float64)
+    n = a.shape[0]
+    A = np.zeros((n, n))
+    A[0, :] = -a
+    A[np.arange(1, n), np.arange(n - 1)] = 1.0
+    return A
+
+
+def companion_run(a, beta, b0, u, x0=None) -> Tuple[np.ndarray, np.ndarray]:
+    """Run the companion state-space system ``(A_c, e_1, beta, b0)`` of one
+    channel over ``u [L]`` from ``x0`` (zeros by default): ``y_t = beta . x_t
+    + b0 u_t`` and ``x_{t+1} = A_c x_t + e_1 u_t`` with the explicit matrix of
+    ``companion_matrix``.  Returns ``y [L]`` and the final state ``[2d]``."""
+    A = companion_matrix(a)
     beta = np.asarray(beta, np.float64)
     u = np.asarray(u, np.float64)
-    n = a.shape[0]
+    n = A.shape[0]
+    e1 = np.zeros(n)
+    e1[0] = 1.0
     x = np.zeros(n) if x0 is None else np.asarray(x0, np.float64).copy()
     y = np.empty(u.shape[0])
     for t in range(u.shape[0]):
-        y[t] = beta @ x + float(b0) * u[t]
-        head = u[t] - a @ x
-        x[1:] = x[:-1].copy()
-        x[0] = head
+        y[t] = float(np.dot(beta, x)) + float(b0) * u[t]
+        x = A @ x + e1 * u[t]
     return y, x
 
 

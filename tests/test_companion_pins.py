@@ -63,20 +63,30 @@ def pin_impulse_response_is_the_modal_filter():
 
 
 def pin_determinant_lemma_numerator():
-    # A = diag(rho), B = 1, C = r: H = [det(zI - A + B C) + (h0 - 1) det(zI - A)] / det(zI - A),
-    # so the numerator is poly(eig(A - B C)) + (h0 - 1) poly(eig(A))
+    # A = diag(rho), B = 1, C = r: by the matrix determinant lemma
+    # det(zI - A + B C) = det(zI - A) (1 + C (zI - A)^-1 B), so the order-2d
+    # numerator of H in z is det(zI - A + B C) + (h0 - 1) det(zI - A) and its
+    # denominator det(zI - A).  Both determinants are evaluated numerically
+    # (np.linalg.det of the explicit matrices) at points z and compared with
+    # the oracle's polynomials, read in z (w = 1/z, times z^2d).
     rng = np.random.default_rng(3)
     lam, R, h0 = rand_modal(rng, 3, 3)
     a, beta, b0 = oc.from_modal(lam, R, h0)
     for c in range(3):
         rho = np.concatenate([lam[c], np.conj(lam[c])]).astype(np.complex128)
         res = np.concatenate([R[c] / 2, np.conj(R[c]) / 2]).astype(np.complex128)
+        n2 = rho.shape[0]
         A = np.diag(rho)
-        BC = np.outer(np.ones(rho.shape[0]), res)
-        num_ref = np.poly(np.linalg.eigvals(A - BC)) + (float(h0[c]) - 1.0) * np.poly(rho)
+        BC = np.outer(np.ones(n2), res)
         num, den = full_coeffs(a[c], beta[c], b0[c])
-        assert np.max(np.abs(num - num_ref)) <= 1e-9 * max(1.0, np.max(np.abs(num_ref))), c
-        assert np.max(np.abs(den - np.poly(np.linalg.eigvals(A)))) <= 1e-10, c
+        for z in (1.3, -0.8 + 0.9j, 2.0j, 0.4 - 1.7j):
+            I = np.eye(n2)
+            num_ref = np.linalg.det(z * I - A + BC) + (float(h0[c]) - 1.0) * np.linalg.det(z * I - A)
+            den_ref = np.linalg.det(z * I - A)
+            num_z = np.polyval(num, z)  # sum_m num[m] z^(2d-m)
+            den_z = np.polyval(den, z)
+            assert abs(num_z - num_ref) <= 1e-9 * max(1.0, abs(num_ref)), (c, z)
+            assert abs(den_z - den_ref) <= 1e-10 * max(1.0, abs(den_ref)), (c, z)
 
 
 def pin_single_real_mode_closed_form():

@@ -206,20 +206,36 @@ def pin_lfilter_modal():
 
 
 def pin_transfer_function_route():
-    # rational form of the same system (App. A.6): a = poly(eig(A)),
-    # b = poly(eig(A - B C)) + (h0 - 1) a with A = diag(lam), B = 1, C = R;
-    # the real part of the rational filter's output is y.
+    # the same system as one rational transfer function in w = z^-1: the
+    # partial fractions h0 + sum_n R_n w / (1 - lam_n w) brought over the
+    # common denominator prod_n (1 - lam_n w) (expanded with np.convolve),
+    # checked against the residue form on the unit circle and then run as a
+    # difference equation by scipy.signal.lfilter; the real part of its
+    # output is y (the real part of the modal filter's output)
     rng = np.random.default_rng(3)
-    lam, R, h0, up, ud = rand_case(rng, 1, 2, 3, 60, 10)
+    d = 3
+    lam, R, h0, up, ud = rand_case(rng, 1, 2, d, 60, 10)
     out = oracle.run(lam, R, h0, up, ud)
     for c in range(2):
-        A = np.diag(lam[c].astype(np.complex128))
-        Bv = np.ones((3, 1), np.complex128)
-        Cv = R[c].astype(np.complex128)[None, :]
-        a = np.poly(np.linalg.eigvals(A))
-        bb = np.poly(np.linalg.eigvals(A - Bv @ Cv)) + (float(h0[c]) - 1.0) * a
+        ls = lam[c].astype(np.complex128)
+        rs = R[c].astype(np.complex128)
+        den = np.array([1.0 + 0j])
+        for l in ls:
+            den = np.convolve(den, [1.0, -l])
+        num = float(h0[c]) * den
+        for n in range(d):
+            others = np.array([1.0 + 0j])
+            for j in range(d):
+                if j != n:
+                    others = np.convolve(others, [1.0, -ls[j]])
+            num[1:] += rs[n] * others
+        for om in (0.0, 0.7, 2.1, np.pi):
+            w = np.exp(-1j * om)
+            ref = float(h0[c]) + np.sum(rs * w / (1 - ls * w))
+            got = np.polyval(num[::-1], w) / np.polyval(den[::-1], w)
+            assert abs(got - ref) <= 1e-11 * max(1.0, abs(ref)), (c, om)
         u = np.concatenate([up[0, :, c], ud[0, :, c]]).astype(np.complex128)
-        y = np.real(scipy.signal.lfilter(bb, a, u))
+        y = np.real(scipy.signal.lfilter(num, den, u))
         ref = np.concatenate([out["y_prefill"][0, :, c], out["y_dec"][0, :, c]])
         assert relerr(ref, y) < 1e-8
 
@@ -294,8 +310,48 @@ def pin_invariants():
     np.testing.assert_allclose(full["x_T"], o1["x_end"], rtol=1e-12, atol=1e-12)
 
 
+def pin_conv_at():
+    # one output of eq. "cnn" against numpy's full convolution (a library
+    # route that shares nothing with the oracle), at the first lags, a middle
+    # one and the last, on random rows, plus a hand-worked example:
+    # h = (1, 2, 3), u = (4, 5, 6): y_0 = 4, y_1 = 2*4 + 5 = 13,
+    # y_2 = 3*4 + 2*5 + 6 = 28
+    assert oracle.conv_at([1.0, 2.0, 3.0], [4.0, 5.0, 6.0], 0) == 4.0
+    assert oracle.conv_at([1.0, 2.0, 3.0], [4.0, 5.0, 6.0], 1) == 13.0
+    assert oracle.conv_at([1.0, 2.0, 3.0], [4.0, 5.0, 6.0], 2) == 28.0
+    rng = np.random.default_rng(12)
+    for L in (1, 2, 7, 300, 4097):
+        h = rng.standard_normal(L)
+        u = rng.standard_normal(L)
+        full = np.convolve(h, u)
+        for t in sorted({0, 1 % L, L // 2, L - 1}):
+            got = oracle.conv_at(h, u, t)
+            assert abs(got - full[t]) <= 1e-12 * max(1.0, float(np.sum(np.abs(h[: t + 1]))) *
+                                                      float(np.max(np.abs(u)))), (L, t)
+
+
+def pin_run_rows_subset():
+    # run_rows on a shuffled subset with repeated channels and batch rows must
+    # return, in the order asked, each row's results as the plain-Python
+    # recurrence gives them (no reference to the oracle's own helpers)
+    rng = np.random.default_rng(13)
+    B, D, d, T, K = 3, 5, 3, 25, 6
+    lam, R, h0, up, ud = rand_case(rng, B, D, d, T, K)
+    rows = [(2, 4), (0, 1), (2, 4), (1, 0), (0, 3), (1, 1), (2, 0)]
+    out = oracle.run_rows(lam, R, h0, up, ud, rows)
+    for i, (b, c) in enumerate(rows):
+        u = np.concatenate([up[b, :, c], ud[b, :, c]])
+        ys, xs = brute_recurrence(lam[c], R[c], h0[c], u)
+        ys = np.array(ys)
+        np.testing.assert_allclose(out["y_prefill"][i], ys[:T], rtol=1e-11, atol=1e-11)
+        np.testing.assert_allclose(out["y_dec"][i], ys[T:], rtol=1e-11, atol=1e-11)
+        np.testing.assert_allclose(out["x_T"][i], np.array(xs[T]), rtol=1e-11, atol=1e-11)
+        np.testing.assert_allclose(out["x_end"][i], np.array(xs[T + K]), rtol=1e-11, atol=1e-11)
+
+
 PINS = [pin_impulse_polar, pin_step_response, pin_brute_force, pin_lfilter_modal,
-        pin_transfer_function_route, pin_fftconvolve, pin_conjugate_pair, pin_invariants]
+        pin_transfer_function_route, pin_fftconvolve, pin_conjugate_pair, pin_invariants,
+        pin_conv_at, pin_run_rows_subset]
 GOLDEN_FILES = sorted(glob.glob(os.path.join(GOLDEN, "*.json")))
 
 
@@ -398,9 +454,36 @@ def _conv_no_lag0(h, u):  # drops the j = t term
     return y - np.asarray(h)[..., :1] * np.asarray(u)
 
 
+def _conv_at_lag_shift(h, u, t):  # one lag off: sum_j h[t-1-j] u[j]
+    h = np.asarray(h, np.float64)
+    u = np.asarray(u, np.float64)
+    return float(np.dot(h[t - 1::-1], u[:t])) if t > 0 else 0.0
+
+
+def _run_rows_state_compact_index(lam, R, h0, u_prompt, u_dec, rows):
+    # states from the poles at the row's position among the distinct channels
+    # instead of its own channel (the same on full, in-order row sets)
+    rows = list(rows)
+    out = _orig_run_rows(lam, R, h0, u_prompt, u_dec, rows)
+    chans = sorted({c for _, c in rows})
+    cidx = {c: i for i, c in enumerate(chans)}
+    lam = np.asarray(lam)
+    T = u_prompt.shape[1]
+    for i, (b, c) in enumerate(rows):
+        uf = np.concatenate([u_prompt[b, :, c], u_dec[b, :, c]]).astype(np.float64)
+        out["x_T"][i] = oracle.state_after(lam[cidx[c]], uf, T)
+        out["x_end"][i] = oracle.state_after(lam[cidx[c]], uf, len(uf))
+    return out
+
+
+def _run_rows_sorted(lam, R, h0, u_prompt, u_dec, rows):  # rows returned sorted, not as asked
+    return _orig_run_rows(lam, R, h0, u_prompt, u_dec, sorted(set(rows)) if rows else rows)
+
+
 _orig_taps = oracle.filter_taps
 _orig_state = oracle.state_after
 _orig_conv = oracle.causal_conv
+_orig_run_rows = oracle.run_rows
 
 MUTANTS = {
     "power_t": ("filter_taps", _taps_power_t),
@@ -411,6 +494,9 @@ MUTANTS = {
     "state_T_minus_1": ("state_after", _state_off_by_one),
     "state_reversed": ("state_after", _state_reversed),
     "conv_no_lag0": ("causal_conv", _conv_no_lag0),
+    "conv_at_lag_shift": ("conv_at", _conv_at_lag_shift),
+    "run_rows_state_compact_index": ("run_rows", _run_rows_state_compact_index),
+    "run_rows_sorted": ("run_rows", _run_rows_sorted),
 }
 
 
