@@ -53,7 +53,7 @@
 extern "C" {
 #endif
 
-#define LH_ABI_VERSION 1
+#define LH_ABI_VERSION 2
 
 /* complex64, interleaved real and imaginary parts */
 typedef struct lh_c32 {
@@ -82,10 +82,6 @@ typedef enum lh_status {
 /* Largest supported number of modes per channel. */
 #define LH_MAX_MODES 1024
 
-/* chunk_len values that request the matrix-core prefill plans (see lh_prefill). */
-#define LH_PREFILL_MFMA (-1)
-#define LH_PREFILL_MFMA_SEG (-2)
-
 /* LH_ABI_VERSION of the built library. */
 int lh_abi_version(void);
 
@@ -97,36 +93,16 @@ const char* lh_status_string(lh_status status);
 const char* lh_last_error(void);
 
 /*
- * Workspace bytes lh_prefill needs for these sizes and chunk length
- * (chunk_len as in lh_prefill), for either input type (the larger of the
- * float32 and bfloat16 plans' needs).  Returns 0
- * when the plan needs no workspace and (size_t)-1 when the arguments are
- * invalid.  Pure function of its arguments.
+ * Workspace bytes lh_prefill needs for these sizes, for either input type
+ * (the larger of the float32 and bfloat16 plans' needs).  Returns 0 when the
+ * plan needs no workspace and (size_t)-1 when the arguments are invalid.
+ * Pure function of its arguments; host only.
  */
-size_t lh_prefill_workspace_bytes(int64_t B, int64_t D, int64_t d, int64_t T,
-                                  int64_t chunk_len);
-
-/* Prefill plans (what lh_prefill runs; see chunk_len there). */
-typedef enum {
-    LH_PLAN_SCAN = 0,      /* VALU scan: one sequential pass or parallel time chunks */
-    LH_PLAN_MFMA = 1,      /* matrix-core plan over the whole prompt */
-    LH_PLAN_MFMA_SEG = 2   /* segmented matrix-core plan */
-} lh_prefill_plan_kind;
+size_t lh_prefill_workspace_bytes(int64_t B, int64_t D, int64_t d, int64_t T);
 
 /*
- * The plan lh_prefill takes for these sizes, chunk length and input type
- * when u and y are 16-byte aligned (automatic matrix-core plans run the VALU
- * scan, with the same workspace, when they are not).  Returns an
- * lh_prefill_plan_kind, or -1 when the arguments are invalid or no plan
- * exists (as lh_prefill would fail).  Pure function of its arguments; host
- * only, no device call.
- */
-int lh_prefill_plan(int64_t B, int64_t D, int64_t d, int64_t T, int64_t chunk_len,
-                    lh_dtype io_dtype);
-
-/*
- * Prefill: outputs y[b,t,c] for t < T and the post-prompt state
- * state[b,c,n] = x_T (Sec. 3.4, "fast pre-filling"; states start at x_0 = 0).
+ * Prefill (Sec. 3.4, "fast pre-filling"; states start at x_0 = 0): outputs
+ * y[b,t,c] for t < T and the post-prompt state state[b,c,n] = x_T.
  *
  *   lambda, R, h0 : inputs as laid out above
  *   u             : [B,T,D] prompt inputs (io_dtype)
@@ -134,51 +110,100 @@ int lh_prefill_plan(int64_t B, int64_t D, int64_t d, int64_t T, int64_t chunk_le
  *   io_dtype      : LH_F32 or LH_BF16 (u and y)
  *   state         : out, [B,D,d] complex64 (overwritten, not read)
  *   y             : out, [B,T,D] (io_dtype); may be NULL only when T == 0
- *   chunk_len     : 0 = automatic plan; > 0 = the VALU chunked scan with this
- *                   time-chunk length (the prompt is cut into
- *                   ceil(T/chunk_len) chunks processed in parallel; chunk_len
- *                   >= T means one sequential pass per row);
- *                   LH_PREFILL_MFMA = the matrix-core plan (chunks of 32
- *                   steps as dense contractions on the MFMA units; with d =
- *                   16 or 32 the float32 operands are split into bfloat16
- *                   terms, three with float32 u/y, two with bfloat16 u/y,
- *                   and D % 8 == 0 is required; with d = 64 the operands
- *                   stay float32 (16x16x4 float32 products), u/y must be
- *                   float32 and D % 4 == 0; always T >= 1 and 16-byte
- *                   aligned u and y, else LH_ERR_INVALID_ARG).  The
- *                   automatic plan uses it where supported and either
- *                   ceil(D/16) * ceil(B/32) >= 256 (enough workgroups to
- *                   fill the GPU without splitting the prompt in time) or
- *                   an estimate of the chunk steps each compute unit walks
- *                   puts it within 7/5 of the segmented plan below (the
- *                   estimate depends on the input type, so float32 and
- *                   bfloat16 calls may take different plans); at d = 64
- *                   also when T does not split into segments and
- *                   ceil(D/4) * ceil(B/16) >= 256, and never when
- *                   B * T <= 1024 (the VALU scan is faster there);
- *                   LH_PREFILL_MFMA_SEG = the segmented matrix-core plan: the
- *                   prompt is cut into 2^k segments of T / 2^k steps (a
- *                   multiple of 32, at least 256), the fewest whose (batch
- *                   row, segment) pairs fill the GPU; a matrix-core pass
- *                   computes each segment's end state from zero, a carry
- *                   gives each segment its entry state, and a second
- *                   matrix-core pass computes the outputs (same operand
- *                   splitting and requirements as LH_PREFILL_MFMA, and such a
- *                   T).  The automatic plan takes it where the whole-prompt
- *                   matrix-core plan is supported but not chosen and T splits
- *                   this way (at d = 64 only when B * T > 1024)
  *   workspace     : device scratch of at least
- *                   lh_prefill_workspace_bytes(B,D,d,T,chunk_len) bytes,
- *                   256-byte aligned; may be NULL when that size is 0.  Its
- *                   contents on entry are ignored and on exit undefined.
+ *                   lh_prefill_workspace_bytes(B,D,d,T) bytes, 256-byte
+ *                   aligned; may be NULL when that size is 0.  Its contents
+ *                   on entry are ignored and on exit undefined.
+ *
+ * The library picks the plan (lh_prefill_plan with plan = LH_PREFILL_AUTO
+ * reports which): the matrix-core chunked scan over the whole prompt where
+ * its workgroups fill the GPU, the segmented matrix-core plan where the
+ * prompt must be split in time to fill it, else the VALU chunked scan (see
+ * lh_prefill_with_plan for what each computes and needs).  Every plan gives
+ * the same results up to float32 rounding.
  * T == 0 zeroes the state and leaves y untouched.  y must not overlap u,
  * state, lambda, R, h0 or workspace; state must not overlap any input.
  */
 lh_status lh_prefill(const lh_c32* lambda, const lh_c32* R, const float* h0,
                      const void* u, int64_t B, int64_t D, int64_t d, int64_t T,
                      lh_dtype io_dtype, lh_c32* state, void* y,
-                     int64_t chunk_len, void* workspace, size_t workspace_bytes,
-                     void* stream);
+                     void* workspace, size_t workspace_bytes, void* stream);
+
+/* Plan requests of lh_prefill_with_plan (values > 0 are VALU chunk lengths). */
+#define LH_PREFILL_AUTO 0
+#define LH_PREFILL_MFMA (-1)
+#define LH_PREFILL_MFMA_SEG (-2)
+
+/* Prefill plans (what a prefill runs). */
+typedef enum {
+    LH_PLAN_SCAN = 0,      /* VALU scan: one sequential pass or parallel time chunks */
+    LH_PLAN_MFMA = 1,      /* matrix-core plan over the whole prompt */
+    LH_PLAN_MFMA_SEG = 2   /* segmented matrix-core plan */
+} lh_prefill_plan_kind;
+
+/*
+ * The plan a prefill takes for these sizes, plan request and input type when
+ * u and y are 16-byte aligned (automatic matrix-core plans run the VALU scan,
+ * with the same workspace, when they are not).  Returns an
+ * lh_prefill_plan_kind, or -1 when the arguments are invalid or no plan
+ * exists (as the prefill would fail).  Pure function of its arguments; host
+ * only, no device call.
+ */
+int lh_prefill_plan(int64_t B, int64_t D, int64_t d, int64_t T, int64_t plan,
+                    lh_dtype io_dtype);
+
+/*
+ * Workspace bytes of lh_prefill_with_plan for this plan request (as
+ * lh_prefill_workspace_bytes; plan = LH_PREFILL_AUTO gives the same value).
+ */
+size_t lh_prefill_with_plan_workspace_bytes(int64_t B, int64_t D, int64_t d, int64_t T,
+                                            int64_t plan);
+
+/*
+ * lh_prefill with the plan named by the caller instead of chosen by the
+ * library: for callers that compare plans (tests, benchmarks).  Same results,
+ * arguments, ownership and errors as lh_prefill, with
+ *
+ *   plan = LH_PREFILL_AUTO (0): the automatic plan (lh_prefill itself);
+ *   plan > 0: the VALU chunked scan with this time-chunk length (the prompt
+ *            is cut into ceil(T/plan) chunks processed in parallel: each
+ *            chunk's end state from zero, a carry across chunks with
+ *            lambda^plan formed in float64, then the outputs from each chunk's
+ *            entry state; plan >= T means one sequential pass per row);
+ *   plan = LH_PREFILL_MFMA: the matrix-core plan (chunks of 32 steps as dense
+ *            contractions on the MFMA units: outputs Y = T U + W X_in, chunk
+ *            end states S = P U and the carry X_in <- lambda^32 X_in + S; with
+ *            d = 16 or 32 the float32 operands are split into bfloat16 terms,
+ *            three with float32 u/y, two for the outputs and three for the
+ *            state with bfloat16 u/y, and D % 8 == 0 is required; with d = 64
+ *            the operands stay float32 (16x16x4 float32 products), u/y must be
+ *            float32 and D % 4 == 0; always T >= 1 and 16-byte aligned u and
+ *            y, else LH_ERR_INVALID_ARG).  The automatic plan uses it where
+ *            supported and either ceil(D/16) * ceil(B/32) >= 256 (enough
+ *            workgroups to fill the GPU without splitting the prompt in time)
+ *            or an estimate of the chunk steps each compute unit walks puts
+ *            it within 7/5 of the segmented plan below (the estimate depends
+ *            on the input type, so float32 and bfloat16 calls may take
+ *            different plans); at d = 64 also when T does not split into
+ *            segments and ceil(D/4) * ceil(B/16) >= 256, and never when
+ *            B * T <= 1024 (the VALU scan is faster there);
+ *   plan = LH_PREFILL_MFMA_SEG: the segmented matrix-core plan: the prompt is
+ *            cut into 2^k segments of T / 2^k steps (a multiple of 32, at
+ *            least 256), the fewest whose (batch row, segment) pairs fill the
+ *            GPU; a matrix-core pass computes each segment's end state from
+ *            zero, a carry gives each segment its entry state, and a second
+ *            matrix-core pass computes the outputs (same operand splitting
+ *            and requirements as LH_PREFILL_MFMA, and such a T).  The
+ *            automatic plan takes it where the whole-prompt matrix-core plan
+ *            is supported but not chosen and T splits this way (at d = 64
+ *            only when B * T > 1024).
+ * workspace: at least lh_prefill_with_plan_workspace_bytes(B,D,d,T,plan)
+ * bytes.  A plan request the sizes do not support returns LH_ERR_INVALID_ARG.
+ */
+lh_status lh_prefill_with_plan(const lh_c32* lambda, const lh_c32* R, const float* h0,
+                               const void* u, int64_t B, int64_t D, int64_t d, int64_t T,
+                               lh_dtype io_dtype, lh_c32* state, void* y, int64_t plan,
+                               void* workspace, size_t workspace_bytes, void* stream);
 
 /* Longest prompt lh_prefill_fft accepts (transforms of at most 2^20 points). */
 #define LH_FFT_MAX_T (INT64_C(1) << 19)
@@ -203,7 +228,7 @@ size_t lh_prefill_fft_workspace_bytes(int64_t B, int64_t D, int64_t d, int64_t T
  *   state[b,c,n] = sum_{k<T} lambda[c,n]^(T-1-k) u[b,k,c]  (Vandermonde
  *       contraction)
  *
- * Arguments, layouts, ownership and errors as lh_prefill (no chunk_len), with
+ * Arguments, layouts, ownership and errors as lh_prefill, with
  *   T          : 0 <= T <= LH_FFT_MAX_T
  *   workspace  : at least lh_prefill_fft_workspace_bytes(B,D,d,T) bytes,
  *                256-byte aligned (NULL allowed when that size is 0)

@@ -7,6 +7,7 @@ kernels; there is no fallback.  PyTorch provides device memory and streams.
 
     prefill(lam, R, h0, u, state, y)   # y[b,t,c], t < T, and state = x_T
     prefill_plan(B, D, d, T, io="bf16")  # which plan prefill takes ("scan", "mfma", "mfma_seg")
+    prefill_with_plan(lam, R, h0, u, state, y, plan=PLAN_MFMA)  # a named plan (tests, benchmarks)
     prefill_fft(lam, R, h0, u, state, y)  # the same results by FFT convolution
     step(lam, R, h0, state, u_t, y_t)  # y_t from x_t, then x_{t+1} in place
 
@@ -29,7 +30,11 @@ __all__ = [
     "workspace_bytes",
     "prefill_plan",
     "PREFILL_PLANS",
+    "PLAN_AUTO",
+    "PLAN_MFMA",
+    "PLAN_MFMA_SEG",
     "prefill",
+    "prefill_with_plan",
     "fft_workspace_bytes",
     "prefill_fft",
     "step",
@@ -47,6 +52,10 @@ _LIB_PATH = os.path.join(_HERE, "liblh.so")
 
 LH_F32 = 0
 LH_BF16 = 1
+# plan requests of prefill_with_plan (values > 0 are VALU chunk lengths)
+PLAN_AUTO = 0
+PLAN_MFMA = -1
+PLAN_MFMA_SEG = -2
 STATUS = {
     0: "LH_OK",
     1: "LH_ERR_INVALID_ARG",
@@ -88,13 +97,17 @@ def lib() -> ctypes.CDLL:
     L.lh_status_string.restype = ctypes.c_char_p
     L.lh_last_error.argtypes = []
     L.lh_last_error.restype = ctypes.c_char_p
-    L.lh_prefill_workspace_bytes.argtypes = [i64, i64, i64, i64, i64]
+    L.lh_prefill_workspace_bytes.argtypes = [i64, i64, i64, i64]
     L.lh_prefill_workspace_bytes.restype = sz
+    L.lh_prefill_with_plan_workspace_bytes.argtypes = [i64, i64, i64, i64, i64]
+    L.lh_prefill_with_plan_workspace_bytes.restype = sz
     L.lh_prefill_plan.argtypes = [i64, i64, i64, i64, i64, ctypes.c_int]
     L.lh_prefill_plan.restype = ctypes.c_int
-    L.lh_prefill.argtypes = [vp, vp, vp, vp, i64, i64, i64, i64, ctypes.c_int, vp, vp, i64, vp,
-                             sz, vp]
+    L.lh_prefill.argtypes = [vp, vp, vp, vp, i64, i64, i64, i64, ctypes.c_int, vp, vp, vp, sz, vp]
     L.lh_prefill.restype = ctypes.c_int
+    L.lh_prefill_with_plan.argtypes = [vp, vp, vp, vp, i64, i64, i64, i64, ctypes.c_int, vp, vp,
+                                       i64, vp, sz, vp]
+    L.lh_prefill_with_plan.restype = ctypes.c_int
     L.lh_prefill_fft_workspace_bytes.argtypes = [i64, i64, i64, i64]
     L.lh_prefill_fft_workspace_bytes.restype = sz
     L.lh_prefill_fft.argtypes = [vp, vp, vp, vp, i64, i64, i64, i64, ctypes.c_int, vp, vp, vp, sz,
@@ -123,22 +136,28 @@ def _check(status: int) -> None:
         raise LHError(status, lib().lh_last_error().decode(errors="replace"))
 
 
-def workspace_bytes(B: int, D: int, d: int, T: int, chunk_len: int = 0) -> int:
-    n = lib().lh_prefill_workspace_bytes(B, D, d, T, chunk_len)
+def workspace_bytes(B: int, D: int, d: int, T: int, plan: int = PLAN_AUTO) -> int:
+    """Workspace bytes of ``prefill`` (``lh_prefill_workspace_bytes``), or of
+    ``prefill_with_plan`` with this plan request
+    (``lh_prefill_with_plan_workspace_bytes``)."""
+    if plan == PLAN_AUTO:
+        n = lib().lh_prefill_workspace_bytes(B, D, d, T)
+    else:
+        n = lib().lh_prefill_with_plan_workspace_bytes(B, D, d, T, plan)
     if n == ctypes.c_size_t(-1).value:
-        raise LHError(1, f"invalid sizes B={B} D={D} d={d} T={T} chunk_len={chunk_len}")
+        raise LHError(1, f"invalid sizes B={B} D={D} d={d} T={T} plan={plan}")
     return int(n)
 
 
 PREFILL_PLANS = ("scan", "mfma", "mfma_seg")
 
 
-def prefill_plan(B: int, D: int, d: int, T: int, chunk_len: int = 0, io: str = "f32") -> str:
-    """The plan ``prefill`` takes for 16-byte aligned u and y (``lh_prefill_plan``):
+def prefill_plan(B: int, D: int, d: int, T: int, plan: int = PLAN_AUTO, io: str = "f32") -> str:
+    """The plan a prefill takes for 16-byte aligned u and y (``lh_prefill_plan``):
     "scan" (VALU), "mfma" (matrix cores, whole prompt) or "mfma_seg" (segmented)."""
-    k = lib().lh_prefill_plan(B, D, d, T, chunk_len, {"f32": 0, "bf16": 1}[io])
+    k = lib().lh_prefill_plan(B, D, d, T, plan, {"f32": 0, "bf16": 1}[io])
     if k < 0:
-        raise LHError(1, f"no prefill plan for B={B} D={D} d={d} T={T} chunk_len={chunk_len} io={io}")
+        raise LHError(1, f"no prefill plan for B={B} D={D} d={d} T={T} plan={plan} io={io}")
     return PREFILL_PLANS[k]
 
 
@@ -167,19 +186,36 @@ def _need(t, name, dtype, shape):
         raise ValueError(f"{name} must be contiguous")
 
 
-def _stream(dev, stream) -> int:
+def _stream(dev, stream):
+    """(torch stream object, raw hipStream_t handle) of ``stream``: None is the
+    device's current stream; a raw handle is wrapped as an external stream."""
     import torch
 
     if stream is None:
         stream = torch.cuda.current_stream(dev)
-    return int(stream.cuda_stream) if hasattr(stream, "cuda_stream") else int(stream)
+    elif not isinstance(stream, torch.cuda.Stream):
+        stream = torch.cuda.ExternalStream(int(stream), device=dev)
+    return stream, int(stream.cuda_stream)
 
 
-def prefill(lam, R, h0, u, state, y, workspace=None, chunk_len: int = 0, stream=None) -> None:
-    """Prompt outputs ``y`` and post-prompt state ``state`` (both overwritten).
+def _scratch(need: int, workspace, dev, stream):
+    """The caller's workspace, or a new one when ``workspace`` is None.  A
+    workspace allocated here comes from torch's caching allocator, whose blocks
+    belong to the current stream; the library enqueues on ``stream``, so the
+    block is marked as used there (record_stream) and is not handed out again
+    before that stream's work on it has completed."""
+    import torch
 
-    ``workspace``: a uint8 CUDA tensor of at least ``workspace_bytes(...)``
-    bytes, or None to have one allocated here with torch."""
+    if need > 0 and workspace is None:
+        workspace = torch.empty(need, dtype=torch.uint8, device=dev)
+        if stream.cuda_stream != torch.cuda.current_stream(dev).cuda_stream:
+            workspace.record_stream(stream)
+    if workspace is None:
+        return workspace, None, 0
+    return workspace, workspace.data_ptr(), workspace.numel() * workspace.element_size()
+
+
+def _prefill_args(lam, R, h0, u, state, y):
     import torch
 
     B, T, D = u.shape
@@ -190,15 +226,31 @@ def prefill(lam, R, h0, u, state, y, workspace=None, chunk_len: int = 0, stream=
     _need(u, "u", u.dtype, (B, T, D))
     _need(state, "state", torch.complex64, (B, D, d))
     _need(y, "y", u.dtype, (B, T, D))
-    io = _io_dtype(u)
-    need = workspace_bytes(B, D, d, T, chunk_len)
-    if need > 0 and workspace is None:
-        workspace = torch.empty(need, dtype=torch.uint8, device=u.device)
-    ws_ptr = workspace.data_ptr() if workspace is not None else None
-    ws_len = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    return B, D, d, T, _io_dtype(u)
+
+
+def prefill(lam, R, h0, u, state, y, workspace=None, stream=None) -> None:
+    """Prompt outputs ``y`` and post-prompt state ``state`` (both overwritten),
+    with the library's automatic plan (``lh_prefill``).
+
+    ``workspace``: a uint8 CUDA tensor of at least ``workspace_bytes(...)``
+    bytes, or None to have one allocated here with torch."""
+    B, D, d, T, io = _prefill_args(lam, R, h0, u, state, y)
+    st, handle = _stream(u.device, stream)
+    workspace, ws_ptr, ws_len = _scratch(workspace_bytes(B, D, d, T), workspace, u.device, st)
     _check(lib().lh_prefill(lam.data_ptr(), R.data_ptr(), h0.data_ptr(), u.data_ptr(), B, D, d, T,
-                            io, state.data_ptr(), y.data_ptr(), chunk_len, ws_ptr, ws_len,
-                            _stream(u.device, stream)))
+                            io, state.data_ptr(), y.data_ptr(), ws_ptr, ws_len, handle))
+
+
+def prefill_with_plan(lam, R, h0, u, state, y, plan: int, workspace=None, stream=None) -> None:
+    """``prefill`` with a named plan (``lh_prefill_with_plan``): ``PLAN_AUTO``,
+    ``PLAN_MFMA``, ``PLAN_MFMA_SEG`` or a VALU chunk length > 0."""
+    B, D, d, T, io = _prefill_args(lam, R, h0, u, state, y)
+    st, handle = _stream(u.device, stream)
+    workspace, ws_ptr, ws_len = _scratch(workspace_bytes(B, D, d, T, plan), workspace, u.device, st)
+    _check(lib().lh_prefill_with_plan(lam.data_ptr(), R.data_ptr(), h0.data_ptr(), u.data_ptr(), B,
+                                      D, d, T, io, state.data_ptr(), y.data_ptr(), plan, ws_ptr,
+                                      ws_len, handle))
 
 
 def fft_workspace_bytes(B: int, D: int, d: int, T: int) -> int:
@@ -211,25 +263,11 @@ def fft_workspace_bytes(B: int, D: int, d: int, T: int) -> int:
 def prefill_fft(lam, R, h0, u, state, y, workspace=None, stream=None) -> None:
     """``prefill``'s results by FFT convolution with the materialised filter
     and a Vandermonde contraction for the state (``lh_prefill_fft``)."""
-    import torch
-
-    B, T, D = u.shape
-    d = lam.shape[1]
-    _need(lam, "lam", torch.complex64, (D, d))
-    _need(R, "R", torch.complex64, (D, d))
-    _need(h0, "h0", torch.float32, (D,))
-    _need(u, "u", u.dtype, (B, T, D))
-    _need(state, "state", torch.complex64, (B, D, d))
-    _need(y, "y", u.dtype, (B, T, D))
-    io = _io_dtype(u)
-    need = fft_workspace_bytes(B, D, d, T)
-    if need > 0 and workspace is None:
-        workspace = torch.empty(need, dtype=torch.uint8, device=u.device)
-    ws_ptr = workspace.data_ptr() if workspace is not None else None
-    ws_len = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    B, D, d, T, io = _prefill_args(lam, R, h0, u, state, y)
+    st, handle = _stream(u.device, stream)
+    workspace, ws_ptr, ws_len = _scratch(fft_workspace_bytes(B, D, d, T), workspace, u.device, st)
     _check(lib().lh_prefill_fft(lam.data_ptr(), R.data_ptr(), h0.data_ptr(), u.data_ptr(), B, D,
-                                d, T, io, state.data_ptr(), y.data_ptr(), ws_ptr, ws_len,
-                                _stream(u.device, stream)))
+                                d, T, io, state.data_ptr(), y.data_ptr(), ws_ptr, ws_len, handle))
 
 
 def step(lam, R, h0, state, u_t, y_t, stream=None) -> None:
@@ -248,7 +286,7 @@ def step(lam, R, h0, state, u_t, y_t, stream=None) -> None:
     io = _io_dtype(u_t)
     _check(lib().lh_step(lam.data_ptr(), R.data_ptr(), h0.data_ptr(), state.data_ptr(),
                          u_t.data_ptr(), y_t.data_ptr(), B, D, d, io,
-                         _stream(u_t.device, stream)))
+                         _stream(u_t.device, stream)[1]))
 
 
 def mh_step(lam, R, h0, state, q, k, v, y, stream=None) -> None:
@@ -270,7 +308,7 @@ def mh_step(lam, R, h0, state, q, k, v, y, stream=None) -> None:
     io = _io_dtype(q)
     _check(lib().lh_mh_step(lam.data_ptr(), R.data_ptr(), h0.data_ptr(), state.data_ptr(),
                             q.data_ptr(), k.data_ptr(), v.data_ptr(), y.data_ptr(), B, M, N, d,
-                            io, _stream(q.device, stream)))
+                            io, _stream(q.device, stream)[1]))
 
 
 def distill(A, theta, R, target, loss, dA, dtheta, dR, hhat=None, stream=None) -> None:
@@ -296,7 +334,7 @@ def distill(A, theta, R, target, loss, dA, dtheta, dR, hhat=None, stream=None) -
     _check(lib().lh_distill(A.data_ptr(), theta.data_ptr(), R.data_ptr(), target.data_ptr(), D, d,
                             L, loss.data_ptr(), dA.data_ptr(), dtheta.data_ptr(), dR.data_ptr(),
                             hhat.data_ptr() if hhat is not None else None,
-                            _stream(A.device, stream)))
+                            _stream(A.device, stream)[1]))
 
 
 def companion_coeffs(lam, R, a, beta, stream=None) -> None:
@@ -310,7 +348,7 @@ def companion_coeffs(lam, R, a, beta, stream=None) -> None:
     _need(a, "a", torch.float64, (D, 2 * d))
     _need(beta, "beta", torch.float64, (D, 2 * d))
     _check(lib().lh_companion_coeffs(lam.data_ptr(), R.data_ptr(), D, d, a.data_ptr(),
-                                     beta.data_ptr(), _stream(lam.device, stream)))
+                                     beta.data_ptr(), _stream(lam.device, stream)[1]))
 
 
 def companion_step(a, beta, h0, state, u_t, y_t, stream=None) -> None:
@@ -329,7 +367,7 @@ def companion_step(a, beta, h0, state, u_t, y_t, stream=None) -> None:
         raise ValueError(f"companion order must be even (2d), got {order}")
     _check(lib().lh_companion_step(a.data_ptr(), beta.data_ptr(), h0.data_ptr(), state.data_ptr(),
                                    u_t.data_ptr(), y_t.data_ptr(), B, D, order // 2,
-                                   _io_dtype(u_t), _stream(u_t.device, stream)))
+                                   _io_dtype(u_t), _stream(u_t.device, stream)[1]))
 
 
 def companion_init_workspace_bytes(D: int, d: int, T: int) -> int:
@@ -351,10 +389,8 @@ def companion_init(a, u, state, workspace=None, stream=None) -> None:
     _need(state, "state", torch.float64, (B, D, order))
     if order % 2:
         raise ValueError(f"companion order must be even (2d), got {order}")
-    need = companion_init_workspace_bytes(D, order // 2, T)
-    if need > 0 and workspace is None:
-        workspace = torch.empty(need, dtype=torch.uint8, device=u.device)
-    ws_ptr = workspace.data_ptr() if workspace is not None else None
-    ws_len = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    st, handle = _stream(u.device, stream)
+    workspace, ws_ptr, ws_len = _scratch(companion_init_workspace_bytes(D, order // 2, T), workspace,
+                                         u.device, st)
     _check(lib().lh_companion_init(a.data_ptr(), u.data_ptr(), B, D, order // 2, T, _io_dtype(u),
-                                   state.data_ptr(), ws_ptr, ws_len, _stream(u.device, stream)))
+                                   state.data_ptr(), ws_ptr, ws_len, handle))

@@ -200,29 +200,34 @@ const char* lh_status_string(lh_status s)
 
 const char* lh_last_error(void) { return g_last_error; }
 
-size_t lh_prefill_workspace_bytes(int64_t B, int64_t D, int64_t d, int64_t T, int64_t chunk_len)
+size_t lh_prefill_with_plan_workspace_bytes(int64_t B, int64_t D, int64_t d, int64_t T,
+                                            int64_t plan)
 {
-    if (check_sizes(B, D, d, T) != LH_OK || chunk_len < LH_PREFILL_MFMA_SEG) return (size_t)-1;
+    if (check_sizes(B, D, d, T) != LH_OK || plan < LH_PREFILL_MFMA_SEG) return (size_t)-1;
     lh::PrefillPlan p;
-    if (!lh::make_prefill_plan(B, D, d, T, chunk_len, -1, &p)) return (size_t)-1;
+    if (!lh::make_prefill_plan(B, D, d, T, plan, -1, &p)) return (size_t)-1;
     return p.ws_bytes;
 }
 
-int lh_prefill_plan(int64_t B, int64_t D, int64_t d, int64_t T, int64_t chunk_len,
-                    lh_dtype io_dtype)
+size_t lh_prefill_workspace_bytes(int64_t B, int64_t D, int64_t d, int64_t T)
 {
-    if (check_sizes(B, D, d, T) != LH_OK || chunk_len < LH_PREFILL_MFMA_SEG ||
+    return lh_prefill_with_plan_workspace_bytes(B, D, d, T, LH_PREFILL_AUTO);
+}
+
+int lh_prefill_plan(int64_t B, int64_t D, int64_t d, int64_t T, int64_t plan, lh_dtype io_dtype)
+{
+    if (check_sizes(B, D, d, T) != LH_OK || plan < LH_PREFILL_MFMA_SEG ||
         (io_dtype != LH_F32 && io_dtype != LH_BF16))
         return -1;
     lh::PrefillPlan p;
-    if (!lh::make_prefill_plan(B, D, d, T, chunk_len, io_dtype == LH_BF16 ? 1 : 0, &p)) return -1;
+    if (!lh::make_prefill_plan(B, D, d, T, plan, io_dtype == LH_BF16 ? 1 : 0, &p)) return -1;
     return p.mfma_seg ? LH_PLAN_MFMA_SEG : p.mfma ? LH_PLAN_MFMA : LH_PLAN_SCAN;
 }
 
-lh_status lh_prefill(const lh_c32* lambda, const lh_c32* R, const float* h0, const void* u,
-                     int64_t B, int64_t D, int64_t d, int64_t T, lh_dtype io_dtype,
-                     lh_c32* state, void* y, int64_t chunk_len, void* workspace,
-                     size_t workspace_bytes, void* stream)
+lh_status lh_prefill_with_plan(const lh_c32* lambda, const lh_c32* R, const float* h0,
+                               const void* u, int64_t B, int64_t D, int64_t d, int64_t T,
+                               lh_dtype io_dtype, lh_c32* state, void* y, int64_t plan,
+                               void* workspace, size_t workspace_bytes, void* stream)
 {
     g_last_error[0] = '\0';
     lh_status s;
@@ -230,34 +235,43 @@ lh_status lh_prefill(const lh_c32* lambda, const lh_c32* R, const float* h0, con
         return fail(LH_ERR_INVALID_ARG, "lambda, R, h0 and state must not be NULL");
     if ((s = check_sizes(B, D, d, T)) != LH_OK) return s;
     if (T > 0 && (!u || !y)) return fail(LH_ERR_INVALID_ARG, "u and y must not be NULL when T > 0");
-    if (chunk_len < LH_PREFILL_MFMA_SEG)
+    if (plan < LH_PREFILL_MFMA_SEG)
         return fail(LH_ERR_INVALID_ARG,
-                    "chunk_len must be >= 0, LH_PREFILL_MFMA or LH_PREFILL_MFMA_SEG");
+                    "plan must be >= 0, LH_PREFILL_MFMA or LH_PREFILL_MFMA_SEG");
     if ((s = check_dtype(io_dtype)) != LH_OK) return s;
-    lh::PrefillPlan plan;
-    if (!lh::make_prefill_plan(B, D, d, T, chunk_len, io_dtype == LH_BF16 ? 1 : 0, &plan))
+    lh::PrefillPlan pl;
+    if (!lh::make_prefill_plan(B, D, d, T, plan, io_dtype == LH_BF16 ? 1 : 0, &pl))
         return fail(LH_ERR_INVALID_ARG, "no prefill plan for these sizes%s",
-                    chunk_len == LH_PREFILL_MFMA
+                    plan == LH_PREFILL_MFMA
                         ? " (the matrix-core plan needs T >= 1 and d = 16 or 32 with D % 8 == 0, "
                           "or d = 64 with float32 u/y and D % 4 == 0)"
-                    : chunk_len == LH_PREFILL_MFMA_SEG
+                    : plan == LH_PREFILL_MFMA_SEG
                         ? " (the segmented matrix-core plan also needs T = s * 2^k * 32 "
                           "steps, k >= 1, segments of at least 256 steps)"
                         : "");
-    if (plan.mfma_forced && (reinterpret_cast<uintptr_t>(u) % 16 != 0 ||
-                             reinterpret_cast<uintptr_t>(y) % 16 != 0))
+    if (pl.mfma_forced && (reinterpret_cast<uintptr_t>(u) % 16 != 0 ||
+                           reinterpret_cast<uintptr_t>(y) % 16 != 0))
         return fail(LH_ERR_INVALID_ARG, "the matrix-core plan needs 16-byte aligned u and y");
 
     if ((s = check_prefill_buffers(lambda, R, h0, u, B, D, d, T, io_dtype, state, y, workspace,
-                                   plan.ws_bytes, workspace_bytes)) != LH_OK)
+                                   pl.ws_bytes, workspace_bytes)) != LH_OK)
         return s;
 
     return from_hip(
         lh::launch_prefill(reinterpret_cast<const float2*>(lambda),
                            reinterpret_cast<const float2*>(R), h0, u, io_dtype == LH_BF16, B, D,
-                           d, T, reinterpret_cast<float2*>(state), y, plan, workspace,
+                           d, T, reinterpret_cast<float2*>(state), y, pl, workspace,
                            static_cast<hipStream_t>(stream)),
         "prefill launch");
+}
+
+lh_status lh_prefill(const lh_c32* lambda, const lh_c32* R, const float* h0, const void* u,
+                     int64_t B, int64_t D, int64_t d, int64_t T, lh_dtype io_dtype,
+                     lh_c32* state, void* y, void* workspace, size_t workspace_bytes,
+                     void* stream)
+{
+    return lh_prefill_with_plan(lambda, R, h0, u, B, D, d, T, io_dtype, state, y,
+                                LH_PREFILL_AUTO, workspace, workspace_bytes, stream);
 }
 
 size_t lh_prefill_fft_workspace_bytes(int64_t B, int64_t D, int64_t d, int64_t T)

@@ -51,10 +51,13 @@ struct PrefillPlan {
     size_t off_mfma;  // workspace offset of the matrix-core tables (segmented plan)
 };
 
-// Returns false when the sizes are invalid or overflow.  io: 0 float32, 1
-// bfloat16 u/y, -1 either (the automatic plan may differ between them; the
-// workspace size is then the larger of the two).
-bool make_prefill_plan(int64_t B, int64_t D, int64_t d, int64_t T, int64_t chunk_len, int io,
+// The plan of a prefill call.  request: 0 automatic, > 0 the VALU chunked
+// scan with this chunk length, -1 the matrix-core plan, -2 the segmented
+// matrix-core plan.  Returns false when the sizes are invalid, overflow or do
+// not support the request.  io: 0 float32, 1 bfloat16 u/y, -1 either (the
+// automatic plan may differ between them; the workspace size is then the
+// larger of the two).
+bool make_prefill_plan(int64_t B, int64_t D, int64_t d, int64_t T, int64_t request, int io,
                        PrefillPlan* plan);
 
 // Launchers (asynchronous, on `stream`); they return the launch status.

@@ -287,21 +287,21 @@ inline bool grid_for(int64_t n, dim3* g)
 
 }  // namespace
 
-bool make_prefill_plan(int64_t B, int64_t D, int64_t d, int64_t T, int64_t chunk_len, int io,
+bool make_prefill_plan(int64_t B, int64_t D, int64_t d, int64_t T, int64_t request, int io,
                        PrefillPlan* plan)
 {
     if (io < 0) {  // workspace for either input type
         // (a type with no plan for these sizes, such as bfloat16 under the
         // forced matrix-core plan at d = 64, adds nothing)
         PrefillPlan pf, pb;
-        const bool f = make_prefill_plan(B, D, d, T, chunk_len, 0, &pf);
-        const bool b = make_prefill_plan(B, D, d, T, chunk_len, 1, &pb);
+        const bool f = make_prefill_plan(B, D, d, T, request, 0, &pf);
+        const bool b = make_prefill_plan(B, D, d, T, request, 1, &pb);
         if (!f && !b) return false;
         *plan = f ? pf : pb;
         if (f && b && pb.ws_bytes > plan->ws_bytes) plan->ws_bytes = pb.ws_bytes;
         return true;
     }
-    if (B < 1 || D < 1 || d < 1 || d > 1024 || T < 0 || chunk_len < -2) return false;
+    if (B < 1 || D < 1 || d < 1 || d > 1024 || T < 0 || request < -2) return false;
     // element counts must fit comfortably in int64 (and the byte sizes too)
     const int64_t lim = INT64_C(1) << 58;
     if (B > lim / D || B * D > lim / (T > d ? (T > 0 ? T : 1) : d)) return false;
@@ -319,8 +319,8 @@ bool make_prefill_plan(int64_t B, int64_t D, int64_t d, int64_t T, int64_t chunk
     if (T == 0) {
         p.C = 0;
         p.nchunks = 0;
-    } else if (chunk_len > 0) {
-        p.C = chunk_len < T ? chunk_len : T;
+    } else if (request > 0) {
+        p.C = request < T ? request : T;
         p.nchunks = (T + p.C - 1) / p.C;
     } else {
         // Automatic: keep one sequential pass when the (b, c) rows alone give
@@ -351,18 +351,18 @@ bool make_prefill_plan(int64_t B, int64_t D, int64_t d, int64_t T, int64_t chunk
     // The automatic plan runs on the matrix cores where supported; the
     // workspace also covers the VALU plan above, taken when u or y is not
     // 16-byte aligned.
-    p.mfma_forced = chunk_len == -1 || chunk_len == -2;
+    p.mfma_forced = request == -1 || request == -2;
     if (p.mfma_forced && !mfma_supported(B, D, d, T, io == 1)) return false;
-    const int choice = chunk_len == 0 && mfma_supported(B, D, d, T, io == 1)
+    const int choice = request == 0 && mfma_supported(B, D, d, T, io == 1)
                            ? mfma_auto_plan(B, D, d, T, io == 1)
                            : 0;
-    p.mfma = chunk_len == -1 || choice == 1;
+    p.mfma = request == -1 || choice == 1;
     p.mfma_seg = false;
     p.off_mfma = 0;
     if (p.mfma) {
         const size_t mb = mfma_workspace_bytes(D, d);
         if (p.mfma_forced || mb > p.ws_bytes) p.ws_bytes = mb;  // a forced plan has no fallback
-    } else if (chunk_len == -2 || choice == 2) {
+    } else if (request == -2 || choice == 2) {
         // too few (batch row, channel group) tiles for the whole-prompt matrix-core
         // plan: cut the prompt into segments that run in parallel, on the matrix
         // cores, with the chunked scan's carry in between
@@ -377,7 +377,7 @@ bool make_prefill_plan(int64_t B, int64_t D, int64_t d, int64_t T, int64_t chunk
             const size_t xin_bytes = static_cast<size_t>(B) * nseg * D * d * sizeof(float2);
             p.off_mfma = (p.off_xin + xin_bytes + 255) / 256 * 256;
             p.ws_bytes = p.off_mfma + mfma_workspace_bytes(D, d);
-        } else if (chunk_len == -2) {
+        } else if (request == -2) {
             return false;
         }
     }

@@ -42,9 +42,10 @@ def to_device(lam, R, h0, up, ud, io: str, device="cuda"):
     return t
 
 
-def run_gpu(t, chunk_len: int = 0, ws=None):
-    """Prefill then K decode steps; returns device tensors y [B,T,D], x_T,
-    y_dec [K,B,D], x_end."""
+def run_gpu(t, plan: int = 0, ws=None):
+    """Prefill (lh_prefill, or lh_prefill_with_plan when ``plan`` is not 0)
+    then K decode steps; returns device tensors y [B,T,D], x_T, y_dec [K,B,D],
+    x_end."""
     import torch
 
     import paper_2310_18780_amd as lh
@@ -56,7 +57,10 @@ def run_gpu(t, chunk_len: int = 0, ws=None):
     y = torch.full((B, T, D), float("nan"), dtype=t["u"].dtype, device=dev)
     state = torch.full((B, D, d), complex(float("nan"), float("nan")), dtype=torch.complex64,
                        device=dev)
-    lh.prefill(t["lam"], t["R"], t["h0"], t["u"], state, y, workspace=ws, chunk_len=chunk_len)
+    if plan == 0:
+        lh.prefill(t["lam"], t["R"], t["h0"], t["u"], state, y, workspace=ws)
+    else:
+        lh.prefill_with_plan(t["lam"], t["R"], t["h0"], t["u"], state, y, plan, workspace=ws)
     x_T = state.clone()
     y_dec = torch.full((K, B, D), float("nan"), dtype=t["u"].dtype, device=dev)
     for k in range(K):

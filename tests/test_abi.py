@@ -45,7 +45,8 @@ def no_gpu():
 def test_exports_every_declared_symbol():
     L = lh.lib()
     names = header_functions()
-    assert {"lh_prefill", "lh_step", "lh_prefill_workspace_bytes", "lh_status_string"} <= set(names)
+    assert {"lh_prefill", "lh_step", "lh_prefill_workspace_bytes", "lh_status_string",
+            "lh_prefill_with_plan", "lh_prefill_with_plan_workspace_bytes"} <= set(names)
     for n in names:
         assert hasattr(L, n), f"{n} declared in lh.h but not exported"
 
@@ -67,39 +68,39 @@ def test_abi_version_and_status_strings():
 def test_workspace_sizes():
     # no workspace for T = 0 or a single chunk
     assert lh.workspace_bytes(2, 8, 4, 0) == 0
-    assert lh.workspace_bytes(2, 8, 4, 100, chunk_len=100) == 0
-    assert lh.workspace_bytes(2, 8, 4, 100, chunk_len=500) == 0
+    assert lh.workspace_bytes(2, 8, 4, 100, plan=100) == 0
+    assert lh.workspace_bytes(2, 8, 4, 100, plan=500) == 0
     # chunked: lambda^C table (256-byte aligned) + [B, nchunks, D, d] entry states
     B, D, d, T, C = 3, 10, 4, 100, 30
     nch = -(-T // C)
     pow_bytes = -(-(D * d * 8) // 256) * 256
-    assert lh.workspace_bytes(B, D, d, T, chunk_len=C) == pow_bytes + B * nch * D * d * 8
+    assert lh.workspace_bytes(B, D, d, T, plan=C) == pow_bytes + B * nch * D * d * 8
     # automatic plans: matrix-core tables for d = 16 / 32 with D % 8 == 0
     # (bfloat16 fragments of P, T, W: (4 d/16 + 2) x 3 x 64 x 16 B per channel, plus
     # lambda^C), the VALU plan otherwise (one pass for the wide d = 64 workload)
     frag = lambda D, d: D * (4 * (d // 16) + 2) * 3 * 64 * 16  # noqa: E731
     assert lh.workspace_bytes(64, 2048, 16, 4096) == -(-frag(2048, 16) // 256) * 256 + 2048 * 16 * 8
     # the explicit matrix-core plan needs the same tables
-    assert lh.workspace_bytes(4, 1024, 32, 65536, chunk_len=-1) == frag(1024, 32) + 1024 * 32 * 8
+    assert lh.workspace_bytes(4, 1024, 32, 65536, plan=-1) == frag(1024, 32) + 1024 * 32 * 8
     # long prompt, few rows: the automatic plan cuts the prompt into 32 segments
     # of 2048 steps on the matrix cores (lambda^C, segment entry states, then
     # the matrix-core tables)
     up = lambda x: -(-x // 256) * 256  # noqa: E731
     seg_ws = up(1024 * 32 * 8) + up(4 * 32 * 1024 * 32 * 8) + frag(1024, 32) + 1024 * 32 * 8
     assert lh.workspace_bytes(4, 1024, 32, 65536) == seg_ws
-    assert lh.workspace_bytes(4, 1024, 32, 65536, chunk_len=-2) == seg_ws
+    assert lh.workspace_bytes(4, 1024, 32, 65536, plan=-2) == seg_ws
     # the VALU chunked scan when asked for (32 chunks of 2048 steps)
-    assert lh.workspace_bytes(4, 1024, 32, 65536, chunk_len=2048) == 1024 * 32 * 8 + 4 * 32 * 1024 * 32 * 8
+    assert lh.workspace_bytes(4, 1024, 32, 65536, plan=2048) == 1024 * 32 * 8 + 4 * 32 * 1024 * 32 * 8
     # the segmented plan needs segments of >= 256 steps, a multiple of 32
-    assert lh.lib().lh_prefill_workspace_bytes(4, 1024, 32, 500, -2) == ctypes.c_size_t(-1).value
+    assert lh.lib().lh_prefill_with_plan_workspace_bytes(4, 1024, 32, 500, -2) == ctypes.c_size_t(-1).value
     # the matrix-core plan needs d = 16 / 32 and D % 8 == 0, or d = 64 and D % 4 == 0
     bad = ctypes.c_size_t(-1).value
-    assert lh.lib().lh_prefill_workspace_bytes(2, 12, 16, 64, -1) == bad
-    assert lh.lib().lh_prefill_workspace_bytes(2, 18, 64, 64, -1) == bad
-    assert lh.lib().lh_prefill_workspace_bytes(2, 8, 48, 64, -1) == bad
+    assert lh.lib().lh_prefill_with_plan_workspace_bytes(2, 12, 16, 64, -1) == bad
+    assert lh.lib().lh_prefill_with_plan_workspace_bytes(2, 18, 64, 64, -1) == bad
+    assert lh.lib().lh_prefill_with_plan_workspace_bytes(2, 8, 48, 64, -1) == bad
     # d = 64: float32 blocks of P, T, W (64 + 16 + 64 blocks of 64 lanes x 4 B per
     # channel), then lambda^C
-    assert lh.workspace_bytes(2, 12, 64, 64, chunk_len=-1) == up(12 * 144 * 64 * 4) + 12 * 64 * 8
+    assert lh.workspace_bytes(2, 12, 64, 64, plan=-1) == up(12 * 144 * 64 * 4) + 12 * 64 * 8
     # the wide d = 64 workload: the matrix-core plan with float32 blocks; with
     # bfloat16 u/y (no matrix-core plan at d = 64) one VALU pass
     assert lh.workspace_bytes(256, 2048, 64, 1024) == up(2048 * 144 * 64 * 4) + 2048 * 64 * 8
@@ -112,7 +113,12 @@ def test_workspace_sizes():
     for args in [(0, 1, 1, 1, 0), (1, 0, 1, 1, 0), (1, 1, 0, 1, 0), (1, 1, 1025, 1, 0),
                  (1, 1, 1, -1, 0), (1, 1, 1, 1, -1), (1, 1, 1, 1, -3),
                  (1 << 40, 1 << 20, 64, 1 << 20, 0)]:
-        assert L.lh_prefill_workspace_bytes(*args) == bad, args
+        assert L.lh_prefill_with_plan_workspace_bytes(*args) == bad, args
+        if args[4] == 0:
+            assert L.lh_prefill_workspace_bytes(*args[:4]) == bad, args
+    # the automatic request of the planned call is lh_prefill's own size
+    for args in [(2, 8, 4, 0), (64, 2048, 16, 4096), (4, 1024, 32, 65536), (2, 70, 16, 300)]:
+        assert L.lh_prefill_with_plan_workspace_bytes(*args, 0) == L.lh_prefill_workspace_bytes(*args)
 
 
 def test_prefill_plan_query():
@@ -132,10 +138,10 @@ def test_prefill_plan_query():
     assert P(2, 70, 16, 300) == "scan"                 # D % 8 != 0
     assert P(4, 1024, 32, 500) == "scan"               # T does not split into segments
     # explicit plans
-    assert P(4, 1024, 32, 65536, chunk_len=2048) == "scan"
-    assert P(2, 16, 16, 64, chunk_len=-1) == "mfma"
-    assert P(2, 16, 16, 1024, chunk_len=-2) == "mfma_seg"
-    assert P(2, 12, 64, 64, chunk_len=-1) == "mfma"    # d = 64, float32 u/y
+    assert P(4, 1024, 32, 65536, plan=2048) == "scan"
+    assert P(2, 16, 16, 64, plan=-1) == "mfma"
+    assert P(2, 16, 16, 1024, plan=-2) == "mfma_seg"
+    assert P(2, 12, 64, 64, plan=-1) == "mfma"    # d = 64, float32 u/y
     L = lh.lib()
     for args in [(2, 12, 16, 64, -1, 0), (2, 12, 64, 64, -1, 1), (2, 18, 64, 64, -1, 0), (4, 1024, 32, 500, -2, 0), (0, 1, 1, 1, 0, 0),
                  (1, 1, 1, 1, -3, 0), (1, 1, 1, 1, 0, 2), (1, 1, 1, -1, 0, 1)]:
@@ -148,11 +154,18 @@ MB = 1 << 20
 
 
 def prefill_args(**kw):
+    """Arguments of lh_prefill_with_plan (with the plan request ``chunk``)."""
     a = dict(lam=A, R=A + MB, h0=A + 2 * MB, u=A + 3 * MB, B=2, D=8, d=4, T=16, io=lh.LH_F32,
              state=A + 64 * MB, y=A + 128 * MB, chunk=0, ws=None, ws_bytes=0, stream=None)
     a.update(kw)
     return [a[k] for k in ("lam", "R", "h0", "u", "B", "D", "d", "T", "io", "state", "y", "chunk",
                            "ws", "ws_bytes", "stream")]
+
+
+def auto_args(**kw):
+    """Arguments of lh_prefill (no plan request)."""
+    args = prefill_args(**kw)
+    return args[:11] + args[12:]
 
 
 def step_args(**kw):
@@ -182,15 +195,19 @@ def step_args(**kw):
 ])
 def test_prefill_rejects_bad_arguments(kw, status):
     L = lh.lib()
-    assert L.lh_prefill(*prefill_args(**kw)) == status
+    assert L.lh_prefill_with_plan(*prefill_args(**kw)) == status
     assert L.lh_last_error().decode() != ""
+    if "chunk" not in kw:  # the automatic call checks the same way
+        assert L.lh_prefill(*auto_args(**kw)) == status
+        assert L.lh_last_error().decode() != ""
 
 
 def test_prefill_t0_allows_null_io():
     if not no_gpu():
         pytest.skip("made-up addresses are only passed through when no GPU is visible")
     L = lh.lib()
-    assert L.lh_prefill(*prefill_args(T=0, u=None, y=None)) == 4  # reaches the device check
+    assert L.lh_prefill(*auto_args(T=0, u=None, y=None)) == 4  # reaches the device check
+    assert L.lh_prefill_with_plan(*prefill_args(T=0, u=None, y=None)) == 4
 
 
 @pytest.mark.parametrize("kw,status", [
@@ -210,8 +227,9 @@ def test_valid_arguments_report_no_device_without_gpu():
     if not no_gpu():
         pytest.skip("made-up addresses are only passed through when no GPU is visible")
     L = lh.lib()
-    assert L.lh_prefill(*prefill_args()) == 4
+    assert L.lh_prefill(*auto_args()) == 4
     assert "device" in L.lh_last_error().decode()
+    assert L.lh_prefill_with_plan(*prefill_args()) == 4
     assert L.lh_step(*step_args()) == 4
     assert L.lh_step(*step_args(io=lh.LH_BF16)) == 4
 

@@ -75,7 +75,7 @@ def test_prefill_plans(kind):
     y = torch.empty_like(t["u"])
     state = torch.empty((B, D, d), dtype=torch.complex64, device="cuda")
     if kind == "segmented":
-        assert lh.workspace_bytes(B, D, d, T) > lh.workspace_bytes(B, D, d, T, chunk_len=256)
+        assert lh.workspace_bytes(B, D, d, T) > lh.workspace_bytes(B, D, d, T, plan=256)
         ws = torch.empty(lh.workspace_bytes(B, D, d, T), dtype=torch.uint8, device="cuda")
 
         def run():

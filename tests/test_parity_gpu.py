@@ -45,7 +45,7 @@ def small_case(B, D, d, T, K, io, seed=0, r=(0.5, 0.999), theta=np.pi):
     return w, workloads.make_inputs(w)
 
 
-# (B, D, d, T, K, io, chunk_len)
+# (B, D, d, T, K, io, plan)
 SMALL = [
     (1, 4, 4, 64, 16, "f32", 0),       # the tiny workload's shape, automatic plan
     (2, 70, 16, 300, 20, "f32", 0),    # one sequential pass, D not a multiple of 64
@@ -68,7 +68,7 @@ SMALL = [
     (1, 8, 4, 40, 3, "f32", 39),       # two chunks, last of length 1
     (4, 256, 16, 512, 8, "bf16", 64),  # many waves, bf16, chunked
     (3, 20, 128, 60, 5, "f32", 0),     # d = 128: step with 64 lanes per row
-    # matrix-core prefill (chunk_len = -1 = LH_PREFILL_MFMA; d = 16 / 32, D % 8 == 0)
+    # matrix-core prefill (plan = -1 = LH_PREFILL_MFMA; d = 16 / 32, D % 8 == 0)
     (2, 64, 16, 300, 20, "f32", -1),   # ragged last chunk (300 = 9*32 + 12), 14 idle columns
     (3, 136, 16, 257, 9, "bf16", -1),  # 17 channel groups (partial line group), 257 = 8*32 + 1
     (17, 16, 32, 100, 5, "f32", -1),   # d = 32, second batch block of one row
@@ -92,7 +92,7 @@ SMALL = [
     (5, 67, 2, 33, 6, "bf16", 0),      # d = 2: one lane per row, B not a multiple of 4
     (3, 1, 16, 90, 5, "f32", 0),       # a single channel
     (2, 1, 5, 70, 4, "bf16", 16),      # a single channel, chunked, generic decode
-    # segmented matrix-core prefill (chunk_len = -2 = LH_PREFILL_MFMA_SEG: T cut into
+    # segmented matrix-core prefill (plan = -2 = LH_PREFILL_MFMA_SEG: T cut into
     # 2^k segments of >= 256 steps; each (batch row, segment) pair is a matrix column)
     (2, 64, 16, 512, 5, "f32", -2),    # two segments of 256 steps
     (3, 136, 16, 1024, 5, "bf16", -2), # four segments, 17 channel groups, bfloat16
@@ -118,7 +118,7 @@ def test_small_case(case):
     _log(f"[small] {case}")
     w, (lam, R, h0, up, ud) = small_case(B, D, d, T, K, io)
     ref = oracle.run(lam, R, h0, up, ud)
-    out = run_gpu(to_device(lam, R, h0, up, ud, io), chunk_len=chunk)
+    out = run_gpu(to_device(lam, R, h0, up, ud, io), plan=chunk)
     errs = compare_full(out, ref, io)
     _log(f"[small] {case} max row-relative errors {errs}")
 
@@ -194,8 +194,8 @@ def test_bitwise_determinism():
     lam, R, h0, up, ud = workloads.make_inputs(w.with_(K=32))
     t = to_device(lam, R, h0, up, ud, w.io)
     for chunk in (0, 100):
-        a = run_gpu(t, chunk_len=chunk)
-        b = run_gpu(t, chunk_len=chunk)
+        a = run_gpu(t, plan=chunk)
+        b = run_gpu(t, plan=chunk)
         for k in a:
             assert torch.equal(_bits(a[k]), _bits(b[k])), (chunk, k)
 
@@ -279,7 +279,7 @@ def test_chunk_plans_agree_with_oracle_on_long_prompt():
     ref = oracle.run(lam, R, h0, up, ud)
     t = to_device(lam, R, h0, up, ud, w.io)
     for chunk in (0, 256, 1000, 4096, 16384):
-        out = run_gpu(t, chunk_len=chunk)
+        out = run_gpu(t, plan=chunk)
         _log(f"[long] chunk={chunk} {compare_full(out, ref, w.io)}")
 
 
@@ -367,7 +367,7 @@ def test_automatic_plan_choice(case):
     for ch in (0, want):
         y = torch.full_like(t["u"], float("nan"))
         st = torch.full((B, D, d), complex(float("nan"), 0), dtype=torch.complex64, device="cuda")
-        lh.prefill(t["lam"], t["R"], t["h0"], t["u"], st, y, chunk_len=ch)
+        lh.prefill_with_plan(t["lam"], t["R"], t["h0"], t["u"], st, y, ch)
         torch.cuda.synchronize()
         res[ch] = (y, st)
     assert torch.equal(res[0][0], res[want][0]) and torch.equal(res[0][1], res[want][1])
@@ -398,3 +398,45 @@ def test_batch_past_the_grid_limit():
         torch.cuda.empty_cache()
         ref = oracle.run_rows(lam, R, h0, up, ud, rows)
         _log(f"[grid limit] B={B} errors {compare_rows(got, ref, 'f32')}")
+
+
+def test_prefill_on_a_side_stream_under_allocator_churn():
+    """A prefill enqueued on a stream other than the current one, with its
+    workspace allocated by the binding, keeps that workspace while it runs:
+    allocations and writes on the current stream right after the call (which
+    the caching allocator would serve from a block it thinks free) change no
+    result.  Compared bit for bit with the same call on the current stream,
+    and sampled rows with the oracle."""
+    import torch
+
+    import paper_2310_18780_amd as lh
+
+    B, D, d, T = 16, 512, 16, 2048  # matrix-core plan with a 6 MB workspace
+    w, (lam, R, h0, up, ud) = small_case(B, D, d, T, 0, "f32")
+    t = to_device(lam, R, h0, up, ud, "f32")
+    need = lh.workspace_bytes(B, D, d, T)
+    assert need > 0
+    ref_y = torch.empty_like(t["u"])
+    ref_x = torch.empty((B, D, d), dtype=torch.complex64, device="cuda")
+    lh.prefill(t["lam"], t["R"], t["h0"], t["u"], ref_x, ref_y)
+    torch.cuda.synchronize()
+    side = torch.cuda.Stream()  # default priority
+    for rep in range(3):
+        y = torch.full_like(t["u"], float("nan"))
+        x = torch.full((B, D, d), complex(float("nan"), 0), dtype=torch.complex64, device="cuda")
+        torch.cuda.synchronize()
+        lh.prefill(t["lam"], t["R"], t["h0"], t["u"], x, y, stream=side)
+        for _ in range(8):  # churn on the current stream while the prefill runs
+            junk = torch.empty(need, dtype=torch.uint8, device="cuda")
+            junk.fill_(0x7F)
+            del junk
+        side.synchronize()
+        torch.cuda.synchronize()
+        assert torch.equal(y, ref_y) and torch.equal(x, ref_x), f"repetition {rep}"
+    rows = [(0, 0), (3, 17), (15, 511), (8, 256)]
+    ref = oracle.run_rows(lam, R, h0, up, ud, rows)
+    yg = np.stack([_np(y[b, :, c]) for b, c in rows])
+    xg = np.stack([_np(x[b, c]) for b, c in rows])
+    errs = (check_y(yg, ref["y_prefill"], "f32", "side-stream prefill y"),
+            check_x(xg, ref["x_T"], "side-stream x_T"))
+    _log(f"[side stream] row errors {errs}")

@@ -48,7 +48,7 @@ def _plans(lh, B, D, d, T, io, rng):
     plans = [0, int(rng.integers(1, max(2, T + 1)))]
     for ch in (-1, -2):
         try:
-            lh.prefill_plan(B, D, d, T, chunk_len=ch, io=io)
+            lh.prefill_plan(B, D, d, T, plan=ch, io=io)
         except Exception:
             continue
         plans.append(ch)
@@ -77,7 +77,7 @@ def test_random_shape(case):
     t = to_device(lam, R, h0, up, ud, io)
     rng = np.random.default_rng(1000 + i)
     for ch in _plans(lh, B, D, d, T, io, rng):
-        _log(f"[random] {case} chunk_len={ch}")
-        out = run_gpu(t, chunk_len=ch)
+        _log(f"[random] {case} plan={ch}")
+        out = run_gpu(t, plan=ch)
         errs = compare_full(out, ref, io)
-        _log(f"[random] {case} chunk_len={ch} errors {errs}")
+        _log(f"[random] {case} plan={ch} errors {errs}")
