@@ -48,6 +48,9 @@ def parse():
                    help="(b, c) rows of the oracle sample (0: sized for ~15 s)")
     p.add_argument("--stream-pool", type=int, default=64,
                    help="state buffers of the HBM-streaming decode measurement (0: skip)")
+    p.add_argument("--decode-pool-only", action="store_true",
+                   help="run only the HBM-streaming decode over the state pool (for counter "
+                        "passes of that kernel)")
     p.add_argument("--copy-calibration", action="store_true",
                    help="run only a plain device copy of known size (counter calibration)")
     p.add_argument("--multihead", action="store_true",
@@ -151,6 +154,24 @@ def mfma32_flops(w):
     return 2048 * w.D * -(-w.B // 16) * (144 * full + 80 * part)
 
 
+def dtype_detail(w, plan):
+    """What the arithmetic of the path is, beyond the float32 label."""
+    io = "bfloat16 u/y (widened exactly, outputs rounded to nearest even)" if w.io == "bf16" \
+        else "float32 u/y"
+    if plan == "scan":
+        pre = "prefill on the float32 VALU"
+    elif w.d == 64:
+        pre = "prefill contractions on float32 matrix cores (16x16x4 f32)"
+    elif w.io == "bf16":
+        pre = ("prefill contractions on bfloat16 matrix cores with float32 accumulation: "
+               "float32 operands split into bfloat16 terms, two for the outputs, three for "
+               "the chunk end states; carry in float32")
+    else:
+        pre = ("prefill contractions on bfloat16 matrix cores with float32 accumulation: "
+               "float32 operands split into three bfloat16 terms; carry in float32")
+    return f"complex float32 state; {io}; {pre}; decode on the float32 VALU"
+
+
 def cpu_baseline(w, rows_wanted):
     """The oracle (as it stands) on a bounded sample: complete rows (prompt
     outputs, decode outputs, both states) of (b, c) pairs of the workload."""
@@ -185,6 +206,7 @@ def cpu_baseline(w, rows_wanted):
         "value": seqs * w.K / dt,
         "unit": "tokens/s",
         "cores": oracle.native_threads(),
+        **host_cpu(),
         "kind": "oracle",
         "sample": (f"{len(rows)} (b,c) rows of {w.name} ({seqs:.2f} sequences' worth), each fully "
                    f"computed (T={w.T} prompt + K={w.K} decode outputs by direct float64 "
@@ -193,6 +215,21 @@ def cpu_baseline(w, rows_wanted):
                    f"also produced the prompt outputs in that time"),
         "seconds": dt,
     }
+
+
+def host_cpu():
+    """The host CPUs the oracle may run on: the affinity set's size and the CPU
+    model (``cores`` beside it is the OpenMP thread count the oracle used)."""
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return {"affinity_cpus": len(os.sched_getaffinity(0)), "cpu_model": model}
 
 
 def mh_decode_bytes(w):
@@ -231,6 +268,7 @@ def mh_cpu_baseline(w, seconds=10.0):
         "value": done / w.D * w.K / dt,
         "unit": "tokens/s",
         "cores": oracle.native_threads(),
+        **host_cpu(),
         "kind": "oracle",
         "sample": (f"{done} output rows (b, m, i) of {w.name} (batch rows {bs}), each all "
                    f"T0+K={w.T0 + w.K} steps by direct float64 convolution of its N={w.N} "
@@ -370,7 +408,7 @@ def distill_main(args):
             dt += time.perf_counter() - t1
             done = sl.stop
         cpu = {"value": done * L / dt, "unit": "taps/s", "cores": oracle.native_threads(),
-               "kind": "oracle",
+               **host_cpu(), "kind": "oracle",
                "sample": f"{done} of {w.D} channels (loss and gradients over L={L} taps, "
                          f"d={w.d}, float64 numpy) in {dt:.2f} s",
                "seconds": dt}
@@ -435,7 +473,7 @@ def fft_cpu_baseline(w, seconds=40.0):
     oracle.run_rows(lam, R, h0, up, ud, rows)
     dt = time.perf_counter() - t0
     return {"value": len(rows) / w.D * w.T / dt, "unit": "tokens/s",
-            "cores": oracle.native_threads(), "kind": "oracle",
+            "cores": oracle.native_threads(), **host_cpu(), "kind": "oracle",
             "sample": (f"{len(rows)} (b,c) rows of {w.name} (T={w.T} prompt outputs by direct "
                        f"float64 convolution and the state by direct sums) in {dt:.2f} s; value "
                        f"= prompt tokens per second scaled to whole sequences (rows / D * T / "
@@ -601,7 +639,8 @@ def companion_main(args):
             if time.perf_counter() - t1 > 10.0:
                 break
         dt = time.perf_counter() - t1
-        cpu = {"value": done / D * K / dt, "unit": "tokens/s", "cores": 1, "kind": "oracle",
+        cpu = {"value": done / D * K / dt, "unit": "tokens/s", "cores": 1, **host_cpu(),
+               "kind": "oracle",
                "sample": f"{done} (b,c) rows of {w.name}, K={K} companion steps each (float64 "
                          f"numpy, one process) in {dt:.2f} s; value = steps per second scaled "
                          f"to whole sequences (rows / D * K / time)",
@@ -633,6 +672,80 @@ def companion_main(args):
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
+
+
+def decode_pool(w, t, npool, reps, floors=True):
+    """The decode step over a pool of ``npool`` state buffers (``npool`` x the
+    state, larger than the 256 MB Infinity Cache), one launch per buffer in
+    turn, replayed from a graph: every launch reads and writes its state in
+    HBM (each buffer was last touched ``npool`` launches earlier).  u_t and
+    y_t are one slice each, so the launch moves the step's algorithmic bytes
+    with only the state coming from HBM.  With ``floors``, plain torch kernels
+    moving the same state bytes over the same pool are timed the same way: an
+    in-place update of each buffer, and a copy of each buffer into the one half
+    a pool away (last touched ``npool / 2`` launches, 0.5 GiB, earlier)."""
+    import torch
+
+    import paper_2310_18780_amd as lh
+
+    B, D, d = w.B, w.D, w.d
+    pool = [torch.zeros((B, D, d), dtype=torch.complex64, device="cuda") for _ in range(npool)]
+    yk = torch.empty((B, D), dtype=t["u"].dtype, device="cuda")
+    stream = torch.cuda.current_stream()
+
+    def graph_of(fn):
+        fn()
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            fn()
+        g.replay()
+        torch.cuda.synchronize()
+        return g
+
+    def per_launch_us(g):
+        a, c = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        for _ in range(reps):
+            g.replay()
+        c.record(stream)
+        torch.cuda.synchronize()
+        return a.elapsed_time(c) * 1e3 / (reps * npool)
+
+    g = graph_of(lambda: [lh.step(t["lam"], t["R"], t["h0"], s, t["ud"][0], yk) for s in pool])
+    out = {"launch_us": per_launch_us(g), "pool_buffers": npool,
+           "pool_bytes": npool * 8 * B * D * d, "replays": reps}
+    del g
+    if floors:
+        fl = [s.view(torch.float32) for s in pool]
+        g = graph_of(lambda: [f.add_(1.0) for f in fl])
+        out["inplace_add_floor_us"] = per_launch_us(g)
+        del g
+        g = graph_of(lambda: [fl[(i + npool // 2) % npool].copy_(fl[i]) for i in range(npool)])
+        out["copy_floor_us"] = per_launch_us(g)
+        del g
+    del pool
+    torch.cuda.synchronize()
+    return out
+
+
+def len_pool(r):
+    return r["pool_buffers"]
+
+
+def decode_pool_only_main(args):
+    """Only the HBM-streaming decode (``decode_pool`` without the floors), for
+    counter passes of the decode kernel on that pattern."""
+    import paper_2310_18780_amd as lh
+    import workloads
+
+    lh.lib()
+    w = workloads.workload(args.workload)
+    t = make_device_inputs(w.with_(T=1, K=1))
+    r = decode_pool(w, t, args.stream_pool, max(1, args.steps), floors=False)
+    us = r["launch_us"]
+    print(json.dumps({"workload": w.name, "decode_pool": r,
+                      "gbps": decode_bytes(w) / (us * 1e-6) / 1e9}), flush=True)
 
 
 def launch_floor_main(args):
@@ -703,6 +816,9 @@ def main():
         return
     if args.launch_floor:
         launch_floor_main(args)
+        return
+    if args.decode_pool_only:
+        decode_pool_only_main(args)
         return
 
     import torch
@@ -807,37 +923,62 @@ def main():
         "valu_busy": profile_value(f"prefill_{w.name}_sq_counters.txt", "valu_busy_fraction",
                                    pre_digest)})
 
+    # Eager decode: K launches through the binding, one per token (host
+    # argument checks and marshalling included), timed like the graph replay.
+    for k in range(min(K, 8)):
+        lh.step(t["lam"], t["R"], t["h0"], state, t["ud"][k], y_dec[k])
+    torch.cuda.synchronize()
+    a_e, c_e = ev(), ev()
+    t_e = time.perf_counter()
+    a_e.record(stream)
+    decode_eager()
+    c_e.record(stream)
+    torch.cuda.synchronize()
+    eager_us = a_e.elapsed_time(c_e) * 1e3 / K
+    eager_host_us = (time.perf_counter() - t_e) * 1e6 / K
+
     # HBM-streaming decode: the same kernel over a pool of state buffers larger
-    # than the 256 MB Infinity Cache (like the layers of a model), so every
-    # launch reads and writes its state from HBM.
+    # than the 256 MB Infinity Cache (as the states of a model's layers
+    # together are), so that every launch reads and writes its state in HBM;
+    # plain copy and in-place update kernels over the same pool beside it.
     streaming = None
     if args.stream_pool > 0:
-        pool = [torch.zeros((B, D, d), dtype=torch.complex64, device="cuda")
-                for _ in range(args.stream_pool)]
-        yk = torch.empty((B, D), dtype=t["u"].dtype, device="cuda")
-        g2 = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(g2):
-            for s in pool:
-                lh.step(t["lam"], t["R"], t["h0"], s, t["ud"][0], yk)
-        g2.replay()
-        torch.cuda.synchronize()
-        a, c = ev(), ev()
-        reps = 8
-        a.record(stream)
-        for _ in range(reps):
-            g2.replay()
-        c.record(stream)
-        torch.cuda.synchronize()
-        us = a.elapsed_time(c) * 1e3 / (reps * len(pool))
-        streaming = {"launch_us": us, "gbps": dbytes / (us * 1e-6) / 1e9,
-                     "frac": dbytes / (us * 1e-6) / 1e9 / HBM_PEAK_GBS,
-                     "pool_buffers": len(pool),
-                     "pool_bytes": len(pool) * 8 * B * D * d}
-        del pool, g2
+        streaming = decode_pool(w, t, args.stream_pool, 8)
+        streaming["gbps"] = dbytes / (streaming["launch_us"] * 1e-6) / 1e9
+        streaming["frac"] = streaming["gbps"] / HBM_PEAK_GBS
+        streaming["state_bytes_gbps_of_copy_floor"] = (
+            16 * B * D * d / (streaming["copy_floor_us"] * 1e-6) / 1e9)
 
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(w, args.cpu_rows)
+
+    # The decode kernel's roofline: HBM, taken on the pool pass where the state
+    # streams from HBM; the timed workload's own decode (one 16 MiB state
+    # stepped K times) keeps its state in the Infinity Cache, so its rate is
+    # reported beside it, labelled with that residency.
+    dig = src_digest("decode.hip", "lh_internal.hpp")
+    resident = {"bound": "hbm", "achieved": dec_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": dec_gbs / HBM_PEAK_GBS, "traffic": traffic,
+                "traffic_gbps": (traffic / (dec_launch_us * 1e-6) / 1e9
+                                 if traffic is not None else None),
+                "kernel": "step_pairs_kernel", "bytes_per_launch": dbytes,
+                "launch_us": dec_launch_us,
+                "residency": "infinity-cache: the workload's one state is stepped K times in a "
+                             "row and stays in the 256 MB cache; counters include cache hits"}
+    if streaming is not None:
+        traffic_pool = counter_traffic(f"decode_step_{w.name}_pool_counters.txt", dig)
+        roofline = {"bound": "hbm", "achieved": streaming["gbps"], "peak": HBM_PEAK_GBS,
+                    "unit": "GB/s", "frac": streaming["frac"], "traffic": traffic_pool,
+                    "kernel": "step_pairs_kernel", "bytes_per_launch": dbytes,
+                    "launch_us": streaming["launch_us"],
+                    "copy_floor_us": streaming["copy_floor_us"],
+                    "inplace_add_floor_us": streaming["inplace_add_floor_us"],
+                    "residency": f"hbm: one launch per buffer of a {len_pool(streaming)}-buffer "
+                                 f"state pool ({streaming['pool_bytes'] / 2**30:.2f} GiB), timed "
+                                 f"over {streaming['replays']} graph replays"}
+    else:
+        roofline = resident
 
     out = {
         "metric": METRIC,
@@ -851,6 +992,7 @@ def main():
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "f32",
+        "dtype_detail": dtype_detail(w, plan),
         "data": "synthetic",
         "config": {"workload": w.name, "B": B, "D": D, "d": d, "T": T, "K": K, "io": w.io,
                    "decode_launch": args.decode_launch, "prefill_workspace_bytes": wsb},
@@ -859,11 +1001,10 @@ def main():
         "decode_ms_per_step_total": dec_avg,
         "decode_us_per_token_step": dec_launch_us,
         "decode_gbps": dec_gbs,
-        "roofline": {"bound": "hbm", "achieved": dec_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": dec_gbs / HBM_PEAK_GBS, "traffic": traffic,
-                     "traffic_gbps": (traffic / (dec_launch_us * 1e-6) / 1e9
-                                      if traffic is not None else None),
-                     "kernel": "step_pairs_kernel", "bytes_per_launch": dbytes},
+        "decode_eager_us_per_token_step": eager_us,
+        "decode_eager_host_us_per_token_step": eager_host_us,
+        "roofline": roofline,
+        "roofline_cache_resident": resident,
         "roofline_prefill": roofline_prefill,
         "decode_hbm_streaming": streaming,
         "cpu_baseline": cpu,

@@ -12,18 +12,29 @@
 // d/2 mode pairs of a (b, c) row sit on LPR = d/2 consecutive lanes, one
 // 16-byte access each, so a wavefront reads and writes one contiguous span
 // of the state; the row sum is a butterfly over those lanes (DPP within 16
-// lanes).  Each thread serves NB = 4 batch rows of the same (c, mode pair):
-// lambda and R are loaded once for the four rows, and every thread has four
-// independent 16-byte state loads in flight before it computes.  State loads
-// are ordinary; state stores and the outputs y_t are non-temporal (written
-// once, not re-read by this kernel). Workgroups are ordered channel tile
-// fastest, with the tile count padded to a multiple of 8: workgroup i runs
-// on XCD i mod 8, so every channel tile (its lambda/R and its slice of the
-// state) is served by one XCD's L2 for all batch groups.  Measured against
-// the batch-group-fastest order, this order is faster whenever the state or
-// u_t comes from HBM rather than the Infinity Cache (inputs u_t prepared
-// long before the step, or a model whose layer states together exceed the
-// 256 MB cache); it is slower only when all operands are already cached.
+// lanes).  Each thread serves NB = 8 batch rows of the same (c, mode pair):
+// lambda and R are loaded once for the eight rows, and every thread has
+// eight independent 16-byte state loads in flight before it computes.  A
+// workgroup is one wavefront (64 / LPR channels x 8 batch rows).
+//
+// Cache policy: the state is written with the non-temporal hint, and read
+// with it when the whole state fits the L2s (at most kStreamStateBytes, 32
+// MiB across the 8 XCDs).  An in-place pass that reads its lines with
+// ordinary loads leaves them in the caches to be written back later; a state
+// streaming from HBM (as the states of a model's layers together do) then
+// runs about a quarter slower than a copy of the same bytes, and with
+// non-temporal loads at the copy's rate.  A state that fits the L2s and is
+// stepped again right away stays there either way (within 1%).  A larger
+// state stepped again right away keeps part of itself in the 256 MB Infinity
+// Cache only when read with ordinary loads (a 256 MiB state: 76 us per step
+// against 87 us), so those take ordinary loads.  y_t is stored with ordinary
+// stores: its 16-byte pieces per wavefront and batch row are merged into
+// whole lines in the L2 before they reach HBM.
+//
+// Workgroups are ordered so that XCD x (workgroup i runs on XCD i mod 8)
+// owns one contiguous range of channel tiles: its lambda / R rows, its slice
+// of every batch row of the state, and whole 128-byte lines of u_t and y_t
+// stay with one L2.
 //
 // Generic path (any other d): lanes take single modes j, j + LPR, ...
 // (LPR = next power of two >= d, <= 64) or pairs, one batch row per thread.
@@ -32,9 +43,11 @@
 namespace lh {
 namespace {
 
-constexpr int kBlock = 256;
+constexpr int kBlock = 256;      // generic path
+constexpr int kPairsBlock = 64;  // fast path: one wavefront per workgroup
 constexpr int kXcds = 8;
-constexpr int kRowsPerThread = 4;
+constexpr int kRowsPerThread = 8;
+constexpr int64_t kStreamStateBytes = INT64_C(32) << 20;  // non-temporal state loads up to this size
 
 typedef float f4v __attribute__((ext_vector_type(4)));
 
@@ -117,18 +130,20 @@ __device__ __forceinline__ float re_dot_pair(float4 r, float4 x)
 }
 
 // Fast path: LPR = d / 2 lanes per row, NB rows per thread, 2-D grid of
-// (channel tile, batch group) blocks, blockIdx.x = channel tile with gridDim.x
-// a multiple of 8, so no integer division is needed to place a block.
-template <typename IO, int LPR>
-__global__ __launch_bounds__(kBlock) void step_pairs_kernel(
+// (channel tile, batch group) workgroups.  gridDim.x is the tile count padded
+// to a multiple of 8; workgroup x runs on XCD x % 8, which owns tiles
+// [(x % 8) T8, (x % 8 + 1) T8) with T8 = gridDim.x / 8.  NTL: non-temporal
+// state loads.
+template <typename IO, int LPR, bool NTL>
+__global__ __launch_bounds__(kPairsBlock) void step_pairs_kernel(
     const float2* __restrict__ lam, const float2* __restrict__ R, const float* __restrict__ h0,
     float2* __restrict__ state, const IO* __restrict__ u, IO* __restrict__ y, int B, int D,
     int ntiles)
 {
     constexpr int NB = kRowsPerThread;
-    constexpr int kRows = kBlock / LPR;  // channels per block
+    constexpr int kRows = kPairsBlock / LPR;  // channels per workgroup
     constexpr int d = 2 * LPR;
-    const int ct = blockIdx.x;  // channel tile
+    const int ct = int(blockIdx.x % kXcds) * int(gridDim.x / kXcds) + int(blockIdx.x / kXcds);
     const int b0 = blockIdx.y * NB;
     if (ct >= ntiles) return;  // padding tiles
     const int j = threadIdx.x % LPR;
@@ -144,7 +159,7 @@ __global__ __launch_bounds__(kBlock) void step_pairs_kernel(
     for (int i = 0; i < NB; ++i) {
         const int b = (b0 + i < B) ? b0 + i : B - 1;
         const int64_t row = int64_t(b) * D + cc;
-        x[i] = load4<false>(state + row * d + 2 * j);
+        x[i] = load4<NTL>(state + row * d + 2 * j);
         uv[i] = io_load(u + row);
     }
     const float hz = h0[cc];
@@ -161,7 +176,7 @@ __global__ __launch_bounds__(kBlock) void step_pairs_kernel(
         if (cvalid && b < B) {
             const int64_t row = int64_t(b) * D + c;
             store4<true>(state + row * d + 2 * j, n4);
-            if (j == 0) io_store_nt(y + row, fmaf(hz, uv[i], acc));
+            if (j == 0) io_store(y + row, fmaf(hz, uv[i], acc));
         }
     }
 }
@@ -218,7 +233,7 @@ __global__ __launch_bounds__(kBlock) void step_generic_kernel(
 // 2-D grid of the fast path; false when it does not fit the grid limits
 bool pairs_grid(int lpr, int64_t B, int64_t D, dim3* g, int* ntiles)
 {
-    const int64_t rows_per_block = kBlock / lpr;
+    const int64_t rows_per_block = kPairsBlock / lpr;
     const int64_t nt = (D + rows_per_block - 1) / rows_per_block;
     const int64_t nbg = (B + kRowsPerThread - 1) / kRowsPerThread;
     const int64_t ntp = (nt + kXcds - 1) / kXcds * kXcds;
@@ -228,7 +243,7 @@ bool pairs_grid(int lpr, int64_t B, int64_t D, dim3* g, int* ntiles)
     return true;
 }
 
-template <typename IO>
+template <typename IO, bool NTL>
 hipError_t launch_pairs(int lpr, dim3 grid, int ntiles, const float2* lam, const float2* R,
                         const float* h0, float2* state, const void* u, void* y, int64_t B,
                         int64_t D, hipStream_t stream)
@@ -236,10 +251,10 @@ hipError_t launch_pairs(int lpr, dim3 grid, int ntiles, const float2* lam, const
     const IO* uu = static_cast<const IO*>(u);
     IO* yy = static_cast<IO*>(y);
     const int b = int(B), dd = int(D);
-#define LH_PAIRS(L)                                                                          \
-    case L:                                                                                  \
-        hipLaunchKernelGGL((step_pairs_kernel<IO, L>), grid, dim3(kBlock), 0, stream, lam, R, \
-                           h0, state, uu, yy, b, dd, ntiles);                                \
+#define LH_PAIRS(L)                                                                           \
+    case L:                                                                                   \
+        hipLaunchKernelGGL((step_pairs_kernel<IO, L, NTL>), grid, dim3(kPairsBlock), 0, stream, \
+                           lam, R, h0, state, uu, yy, b, dd, ntiles);                         \
         break;
     switch (lpr) {
         LH_PAIRS(1)
@@ -301,10 +316,16 @@ hipError_t launch_step(const float2* lam, const float2* R, const float* h0, floa
     const int fast_lpr = static_cast<int>(pairs);
     if (pow2_pairs && aligned16 && B < (INT64_C(1) << 31) && D < (INT64_C(1) << 31) &&
         pairs_grid(fast_lpr, B, D, &grid, &ntiles)) {
-        return bf16_io ? launch_pairs<bf16>(fast_lpr, grid, ntiles, lam, R, h0, state, u_t, y_t,
-                                            B, D, stream)
-                       : launch_pairs<float>(fast_lpr, grid, ntiles, lam, R, h0, state, u_t,
-                                             y_t, B, D, stream);
+        const bool ntl = 8 * B * D * d <= kStreamStateBytes;
+        if (bf16_io)
+            return ntl ? launch_pairs<bf16, true>(fast_lpr, grid, ntiles, lam, R, h0, state, u_t,
+                                                  y_t, B, D, stream)
+                       : launch_pairs<bf16, false>(fast_lpr, grid, ntiles, lam, R, h0, state, u_t,
+                                                   y_t, B, D, stream);
+        return ntl ? launch_pairs<float, true>(fast_lpr, grid, ntiles, lam, R, h0, state, u_t, y_t,
+                                               B, D, stream)
+                   : launch_pairs<float, false>(fast_lpr, grid, ntiles, lam, R, h0, state, u_t,
+                                                y_t, B, D, stream);
     }
     // generic layouts
     int lpr = 1;

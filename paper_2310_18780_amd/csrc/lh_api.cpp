@@ -113,8 +113,10 @@ lh_status check_accessible(const Buf& b, int dev)
     hipDeviceptr_t base = nullptr;
     size_t size = 0;
     if (hipMemGetAddressRange(&base, &size, p) == hipSuccess && base != nullptr) {
+        // compared as offsets from the base so that a reported size near
+        // SIZE_MAX cannot wrap the allocation's end around
         const uintptr_t blo = reinterpret_cast<uintptr_t>(base);
-        if (b.lo < blo || b.hi > blo + size)
+        if (b.lo < blo || b.hi - blo > size)
             return fail(LH_ERR_INVALID_ARG,
                         "%s [%p, +%zu) extends past its allocation [%p, +%zu)", b.name, p,
                         (size_t)(b.hi - b.lo), base, size);

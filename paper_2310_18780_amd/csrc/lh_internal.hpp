@@ -80,8 +80,10 @@ size_t mfma_workspace_bytes(int64_t D, int64_t d);
 // Segment count of the segmented matrix-core plan (0 when T does not split
 // into segments of a multiple of 32 steps, at least 256 long).
 int64_t mfma_segments(int64_t B, int64_t D, int64_t d, int64_t T);
+// Matrix-core tables of the filters into the workspace (bf16_io: only the
+// operand terms the bfloat16 kernels read are written).
 hipError_t launch_mfma_setup(const float2* lam, const float2* R, const float* h0, int64_t D,
-                             int64_t d, void* workspace, hipStream_t stream);
+                             int64_t d, bool bf16_io, void* workspace, hipStream_t stream);
 // One pass of the segmented plan: outputs = false writes each segment's end
 // state from zero into slot k < nseg - 1 of xs [B, nseg, D, d]; outputs = true
 // runs every segment from its entry state in xs, writes y and x_T.

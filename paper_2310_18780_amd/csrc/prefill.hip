@@ -411,7 +411,7 @@ hipError_t launch_prefill(const float2* lam, const float2* R, const float* h0, c
         hipError_t e;
         hipLaunchKernelGGL(pow_kernel, g_pow, dim3(kBlock), 0, stream, lam, lamC, D * d, p.C);
         if ((e = hipGetLastError()) != hipSuccess) return e;
-        if ((e = launch_mfma_setup(lam, R, h0, D, d, mws, stream)) != hipSuccess) return e;
+        if ((e = launch_mfma_setup(lam, R, h0, D, d, bf16_io, mws, stream)) != hipSuccess) return e;
         if ((e = launch_mfma_segment_pass(false, lam, u, bf16_io, B, D, d, T, int(p.nchunks), p.C,
                                           xs, state, y, mws, stream)) != hipSuccess)
             return e;

@@ -55,8 +55,10 @@
 // global access is a 16-byte piece of a whole (row, step) segment of the
 // workgroup's channels.  Barriers order LDS only, so the prefetch stays in
 // flight across them.
-// Workgroups are ordered so that the channel groups sharing 128-byte lines
-// of u and y run on one XCD (workgroup i runs on XCD i mod 8).
+// Workgroups are ordered so that each XCD (workgroup i runs on XCD i mod 8)
+// owns a contiguous range of channel groups for all batch groups: its L2
+// fetches those channels' A operands once, and the channel groups sharing
+// 128-byte lines of u and y run on one XCD.
 //
 // A last chunk shorter than C is computed with zero-padded inputs (causality
 // keeps its outputs exact) and its end state by a VALU recurrence from its
@@ -147,14 +149,15 @@ __device__ __forceinline__ void lds_barrier()
 // ------------------------------------------------------------ setup kernel
 // One workgroup per channel: float64 powers lambda_n^e (e = 0..C) and filter
 // taps in LDS, then the A-operand fragments (rounded to float32, split into
-// kTerms bfloat16 vectors at frag[((c * F + f) * kTerms + term) * 64 + lane])
-// and lambda^C (lamc[c][g][q][i], mode 16 q + 4 g + i).
+// kTerms bfloat16 vectors at frag[((c * F + f) * kTerms + term) * 64 + lane];
+// the T and W fragments get only their first tw_terms terms, the ones the
+// main kernel reads) and lambda^C (lamc[c][g][q][i], mode 16 q + 4 g + i).
 template <int DM>
 __global__ __launch_bounds__(256) void mfma_setup_kernel(const float2* __restrict__ lam,
                                                          const float2* __restrict__ R,
                                                          const float* __restrict__ h0,
                                                          bf16x8* __restrict__ frag,
-                                                         float2* __restrict__ lamc)
+                                                         float2* __restrict__ lamc, int tw_terms)
 {
     constexpr int d = 16 * DM;
     constexpr int F = DM == 4 ? n_frag32(DM) : n_frag(DM);
@@ -247,7 +250,7 @@ __global__ __launch_bounds__(256) void mfma_setup_kernel(const float2* __restric
         bf16x8* dst = frag + (int64_t(c) * F + f) * kTerms * 64 + lane;
         dst[0] = t0;
         dst[64] = t1;
-        dst[128] = t2;
+        if (f < 2 * DM || tw_terms > 2) dst[128] = t2;
     }
 }
 
@@ -290,21 +293,26 @@ __host__ __device__ constexpr int waves_of(int DM) { return DM == 4 ? 4 : 8; }
 
 // LDS element type of the staged u tile and operand term counts: bfloat16
 // inputs are exact in one term and their outputs are rounded to bfloat16, so
-// two-term A operands (relative error near 2^-17) suffice; float32 inputs and
-// A operands take three terms.
+// the output operands T and W take two terms (relative error near 2^-17,
+// invisible after the rounding), while the state operand P keeps three
+// (24 significant bits: the chunk end states, and through the carry x_T, are
+// formed at float32 precision); float32 inputs and every A operand take
+// three terms.
 template <typename IO>
 struct Stage;
 template <>
 struct Stage<bf16> {
     typedef __bf16 T;
     static constexpr int kNTU = 1;
-    static constexpr int kNTA = 2;
+    static constexpr int kNTA = 2;  // T, W
+    static constexpr int kNTP = 3;  // P
 };
 template <>
 struct Stage<float> {
     typedef float T;
     static constexpr int kNTU = kTerms;
     static constexpr int kNTA = kTerms;
+    static constexpr int kNTP = kTerms;
 };
 
 // MODE selects what a column of the MFMA tiles is:
@@ -357,7 +365,9 @@ __global__ __launch_bounds__(64 * waves_of(DM)) void mfma_prefill_kernel(
     constexpr int CW = NW * CPW;
     constexpr int BN = kN * NBG;                      // batch rows per workgroup
     constexpr int NTU = Stage<IO>::kNTU;
-    constexpr int KT = Stage<IO>::kNTA;
+    constexpr int KT = Stage<IO>::kNTA;               // terms of T and W
+    constexpr int KTP = Stage<IO>::kNTP;              // terms of P
+    constexpr int KTX = KTP > KT ? KTP : KT;
     typedef typename Stage<IO>::T ST;
     constexpr int ES = int(sizeof(IO));
     constexpr int CPP = 16 / ES;                      // channels per 16-byte piece
@@ -380,14 +390,21 @@ __global__ __launch_bounds__(64 * waves_of(DM)) void mfma_prefill_kernel(
     __shared__ __attribute__((aligned(16))) uint32_t ystage[PF][MODE == kSegState ? 1 : BN * RS];
     __shared__ __attribute__((aligned(16))) float2 lcs[CW][4][4 * DM];  // lambda^C per channel, lane group
 
-    // ---- workgroup -> (channel group, batch group); logical index lin runs
-    // on XCD lin / per_xcd (workgroup i runs on XCD i mod 8), so consecutive
-    // channel groups, which share the 128-byte lines of u and y, meet in one L2
+    // ---- workgroup -> (channel group, batch group).  The CPL channel groups
+    // whose pieces make up one 128-byte line of u and y form a line group;
+    // logical index lin = (line group * nbg + batch group) * CPL + j, channel
+    // group = line group * CPL + j, runs on XCD lin / per_xcd (workgroup i
+    // runs on XCD i mod 8).  Each XCD thus owns a contiguous range of line
+    // groups for every batch group (its L2 fetches those channels' A operands
+    // once), and the workgroups resident together cover whole lines.
+    constexpr int CPL = 128 / (CW * ES) > 1 ? 128 / (CW * ES) : 1;
     const int hw = blockIdx.x;
     const int lin = (hw % 8) * per_xcd + hw / 8;
-    const int cg = lin % ncg;
-    const int bgw = lin / ncg;
-    if (bgw >= nbg) return;  // whole workgroup exits together
+    const int rest = lin / CPL;
+    const int lg = rest / nbg;
+    const int bgw = rest - lg * nbg;
+    const int cg = lg * CPL + (lin - rest * CPL);
+    if (cg >= ncg) return;  // whole workgroup exits together
     const int c0 = cg * CW;
     const int b0 = bgw * BN;
     // columns ("rows" below): batch rows, or (batch row, segment) pairs
@@ -404,7 +421,7 @@ __global__ __launch_bounds__(64 * waves_of(DM)) void mfma_prefill_kernel(
 
     // ---- A operands and lambda^C of this wave's channels (clamped into range;
     // results of channels >= D are never stored)
-    bf16x8 A[CPW][F][KT];
+    bf16x8 A[CPW][F][KTX];
     float A32[CPW][F32];
 #pragma unroll
     for (int k = 0; k < CPW; ++k) {
@@ -417,7 +434,7 @@ __global__ __launch_bounds__(64 * waves_of(DM)) void mfma_prefill_kernel(
 #pragma unroll
             for (int f = 0; f < F; ++f)
 #pragma unroll
-                for (int s = 0; s < KT; ++s)
+                for (int s = 0; s < (f < 2 * DM ? KTP : KT); ++s)
                     A[k][f][s] = frag[((int64_t(cc) * F + f) * kTerms + s) * 64 + lane];
         }
         if (n < 4 * DM)  // lambda^C of the modes of lane group g (read back by the carry)
@@ -660,21 +677,24 @@ __global__ __launch_bounds__(64 * waves_of(DM)) void mfma_prefill_kernel(
                     for (int q = 0; q < DM; ++q) Sr[k][q] = Si[k][q] = f32x4{0.f, 0.f, 0.f, 0.f};
                 }
 #pragma unroll
-                for (int ia = 0; ia < KT; ++ia)
+                for (int ia = 0; ia < KTX; ++ia)
 #pragma unroll
                     for (int ju = 0; ju < NTU; ++ju) {
-                        if (ia + ju >= KT) continue;
 #pragma unroll
                         for (int k = 0; k < CPW; ++k) {
                             if constexpr (MODE != kSegState) {
+                                if (ia + ju < KT) {
 #pragma unroll
-                                for (int mt = 0; mt < 2; ++mt)
-                                    Y[k][mt] = mfma(A[k][2 * DM + mt][ia], U[k][ju], Y[k][mt]);
+                                    for (int mt = 0; mt < 2; ++mt)
+                                        Y[k][mt] = mfma(A[k][2 * DM + mt][ia], U[k][ju], Y[k][mt]);
+                                }
                             }
+                            if (ia + ju < KTP) {
 #pragma unroll
-                            for (int q = 0; q < DM; ++q) {
-                                Sr[k][q] = mfma(A[k][q][ia], U[k][ju], Sr[k][q]);
-                                Si[k][q] = mfma(A[k][DM + q][ia], U[k][ju], Si[k][q]);
+                                for (int q = 0; q < DM; ++q) {
+                                    Sr[k][q] = mfma(A[k][q][ia], U[k][ju], Sr[k][q]);
+                                    Si[k][q] = mfma(A[k][DM + q][ia], U[k][ju], Si[k][q]);
+                                }
                             }
                         }
                     }
@@ -891,10 +911,12 @@ hipError_t launch_main(const float2* lam, const void* u, void* y, float2* state,
                        int nseg, int64_t seg_len, float2* xs, hipStream_t stream)
 {
     constexpr int CW = waves_of(DM) * cpw_of<IO, DM, MODE>();
+    constexpr int CPL = 128 / (CW * int(sizeof(IO))) > 1 ? 128 / (CW * int(sizeof(IO))) : 1;
     const int64_t sv = MODE == kWhole ? 1 : MODE == kSegState ? nseg - 1 : nseg;
     const int64_t ncg = (D + CW - 1) / CW;
     const int64_t nbg = (B * sv + kN * NBG - 1) / (kN * NBG);
-    const int64_t per_xcd = (ncg * nbg + 7) / 8;  // logical workgroups per XCD
+    const int64_t nlg = (ncg + CPL - 1) / CPL;             // line groups
+    const int64_t per_xcd = (nlg * CPL * nbg + 7) / 8;  // logical workgroups per XCD
     const int64_t grid = 8 * per_xcd;
     if (grid > 0x7fffffff || B * sv > 0x7fffffff) return hipErrorInvalidConfiguration;
     hipLaunchKernelGGL((mfma_prefill_kernel<IO, DM, NBG, MODE>), dim3(uint32_t(grid)),
@@ -1023,7 +1045,7 @@ int mfma_auto_plan(int64_t B, int64_t D, int64_t d, int64_t T, bool bf16_io)
 }
 
 hipError_t launch_mfma_setup(const float2* lam, const float2* R, const float* h0, int64_t D,
-                             int64_t d, void* workspace, hipStream_t stream)
+                             int64_t d, bool bf16_io, void* workspace, hipStream_t stream)
 {
     (void)hipGetLastError();
     const int DM = int(d / 16);
@@ -1031,16 +1053,17 @@ hipError_t launch_mfma_setup(const float2* lam, const float2* R, const float* h0
     bf16x8* frag = static_cast<bf16x8*>(workspace);
     float2* lamc = reinterpret_cast<float2*>(static_cast<char*>(workspace) +
                                              (frag_bytes + 255) / 256 * 256);
+    const int tw = bf16_io ? Stage<bf16>::kNTA : Stage<float>::kNTA;
     if (D > 0x7fffffff) return hipErrorInvalidConfiguration;
     if (DM == 1)
         hipLaunchKernelGGL(mfma_setup_kernel<1>, dim3(uint32_t(D)), dim3(256), 0, stream, lam,
-                           R, h0, frag, lamc);
+                           R, h0, frag, lamc, tw);
     else if (DM == 4)
         hipLaunchKernelGGL(mfma_setup_kernel<4>, dim3(uint32_t(D)), dim3(256), 0, stream, lam,
-                           R, h0, frag, lamc);
+                           R, h0, frag, lamc, tw);
     else
         hipLaunchKernelGGL(mfma_setup_kernel<2>, dim3(uint32_t(D)), dim3(256), 0, stream, lam,
-                           R, h0, frag, lamc);
+                           R, h0, frag, lamc, tw);
     return hipGetLastError();
 }
 
@@ -1049,7 +1072,7 @@ hipError_t launch_prefill_mfma(const float2* lam, const float2* R, const float* 
                                int64_t T, float2* state, void* y, void* workspace,
                                hipStream_t stream)
 {
-    hipError_t e = launch_mfma_setup(lam, R, h0, D, d, workspace, stream);
+    hipError_t e = launch_mfma_setup(lam, R, h0, D, d, bf16_io, workspace, stream);
     if (e != hipSuccess) return e;
     return launch_mode<kWhole>(lam, u, bf16_io, B, D, d, T, state, y, workspace, 1, T, nullptr,
                                stream);

@@ -186,9 +186,26 @@ def compare_rows(got, ref, io: str) -> Dict[str, float]:
     return res
 
 
-def sample_rows(B: int, D: int, n: int, seed: int = 123) -> List[Tuple[int, int]]:
+def sample_rows(B: int, D: int, n: int, seed: int = 123, bn: int = 16,
+                cw: int = 16) -> List[Tuple[int, int]]:
+    """At least ``n`` (b, c) rows: the first and last row of the first,
+    second, middle and last block of ``bn`` batch rows crossed with the first
+    and last channel of the first, second, middle and last group of ``cw``
+    channels (the tile edges of the matrix-core plans), the four corners, then
+    random rows."""
     rng = np.random.default_rng(seed)
+
+    def edges(n_items, size):
+        nblk = -(-n_items // size)
+        out = set()
+        for k in {0, 1, nblk // 2, nblk - 1}:
+            if 0 <= k < nblk:
+                out.add(k * size)
+                out.add(min(k * size + size - 1, n_items - 1))
+        return sorted(out)
+
     rows = {(0, 0), (B - 1, D - 1), (0, D - 1), (B - 1, 0)}
+    rows |= {(b, c) for b in edges(B, bn) for c in edges(D, cw)}
     while len(rows) < min(n, B * D):
         rows.add((int(rng.integers(B)), int(rng.integers(D))))
     return sorted(rows)

@@ -134,7 +134,8 @@ def test_tiny_workload():
 @pytest.mark.parametrize("name", ["c2", "c3", "c4", "c5"])
 def test_full_workload_sampled_rows(name):
     """Full-size workload, automatic plan (as benchmarked): every output and
-    state of sampled (b, c) rows against the oracle."""
+    state of at least 128 sampled (b, c) rows against the oracle, among them
+    the first and last rows and channels of several matrix-core tiles."""
     import torch
 
     w = workloads.workload(name)
@@ -142,7 +143,7 @@ def test_full_workload_sampled_rows(name):
     lam, R, h0, up, ud = workloads.make_inputs(w)
     t = to_device(lam, R, h0, up, ud, w.io)
     out = run_gpu(t)
-    rows = sample_rows(w.B, w.D, 24)
+    rows = sample_rows(w.B, w.D, 128)
     got = gather_rows(out, rows)
     del out, t
     torch.cuda.empty_cache()
@@ -374,15 +375,16 @@ def test_automatic_plan_choice(case):
 
 
 def test_batch_past_the_grid_limit():
-    """B = 4 * 65535 + 1 rows: the decode step's fast path would need 65536
-    row groups in the grid's y dimension, so the step takes the generic path;
-    B = 4 * 65535 is the largest fast-path batch.  Sampled rows (both ends and
-    the rows around the row-group boundaries) against the oracle."""
+    """B = 8 * 65535 + 1 rows: the decode step's fast path (8 batch rows per
+    thread) would need 65536 row groups in the grid's y dimension, so the step
+    takes the generic path; B = 8 * 65535 is the largest fast-path batch.
+    Sampled rows (both ends and the rows around the row-group boundaries)
+    against the oracle."""
     import torch
 
     import paper_2310_18780_amd as lh
 
-    for B in (4 * 65535, 4 * 65535 + 1):
+    for B in (8 * 65535, 8 * 65535 + 1):
         D, d, T, K = 1, 2, 3, 2
         w = workloads.Workload("case", B, D, d, T, K, "f32", 0.5, 0.999, np.pi, 1.0 / d, 0)
         lam, R, h0 = workloads.make_params(w)
@@ -390,7 +392,7 @@ def test_batch_past_the_grid_limit():
         up = rng.standard_normal((B, T, D)).astype(np.float32)
         ud = rng.standard_normal((B, K, D)).astype(np.float32)
         out = run_gpu(to_device(lam, R, h0, up, ud, "f32"))
-        bs = sorted({0, 1, 2, 3, 4, B - 5, B - 4, B - 3, B - 2, B - 1,
+        bs = sorted({0, 1, 2, 7, 8, 9, B - 9, B - 8, B - 7, B - 2, B - 1,
                      *rng.integers(B, size=200).tolist()})
         rows = [(b, 0) for b in bs]
         got = gather_rows(out, rows)
