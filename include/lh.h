@@ -129,6 +129,28 @@ lh_status lh_prefill(const lh_c32* lambda, const lh_c32* R, const float* h0,
                      lh_dtype io_dtype, lh_c32* state, void* y,
                      void* workspace, size_t workspace_bytes, void* stream);
 
+/* Scratch bytes lh_prefill_noalloc holds per GPU (64 MiB). */
+#define LH_NOALLOC_SCRATCH_BYTES (UINT64_C(64) << 20)
+
+/*
+ * lh_prefill for callers that cannot allocate device memory (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid allocation): the
+ * same results, arguments, plan, ownership and errors as lh_prefill, with no
+ * workspace argument.  The plan's scratch is a static array of
+ * LH_NOALLOC_SCRATCH_BYTES that the library holds on each GPU it runs on
+ * until the process ends; this call allocates nothing and makes no
+ * allocating runtime call.  Sizes whose plan needs more scratch than that
+ * (lh_prefill_workspace_bytes(B,D,d,T) > LH_NOALLOC_SCRATCH_BYTES) return
+ * LH_ERR_WORKSPACE before anything is enqueued.  Every call on one GPU shares
+ * that GPU's array, which keeps the last call's contents (no plan reads
+ * scratch it has not written in the same call): calls that overlap on one
+ * GPU (on different streams, or from several threads without ordering) race
+ * on it and must not be made.
+ */
+lh_status lh_prefill_noalloc(const lh_c32* lambda, const lh_c32* R, const float* h0,
+                             const void* u, int64_t B, int64_t D, int64_t d, int64_t T,
+                             lh_dtype io_dtype, lh_c32* state, void* y, void* stream);
+
 /* Plan requests of lh_prefill_with_plan (values > 0 are VALU chunk lengths). */
 #define LH_PREFILL_AUTO 0
 #define LH_PREFILL_MFMA (-1)

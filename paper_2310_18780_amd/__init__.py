@@ -35,6 +35,8 @@ __all__ = [
     "PLAN_MFMA_SEG",
     "prefill",
     "prefill_with_plan",
+    "prefill_noalloc",
+    "NOALLOC_SCRATCH_BYTES",
     "fft_workspace_bytes",
     "prefill_fft",
     "step",
@@ -56,6 +58,8 @@ LH_BF16 = 1
 PLAN_AUTO = 0
 PLAN_MFMA = -1
 PLAN_MFMA_SEG = -2
+# scratch that lh_prefill_noalloc holds per GPU
+NOALLOC_SCRATCH_BYTES = 64 << 20
 STATUS = {
     0: "LH_OK",
     1: "LH_ERR_INVALID_ARG",
@@ -108,6 +112,8 @@ def lib() -> ctypes.CDLL:
     L.lh_prefill_with_plan.argtypes = [vp, vp, vp, vp, i64, i64, i64, i64, ctypes.c_int, vp, vp,
                                        i64, vp, sz, vp]
     L.lh_prefill_with_plan.restype = ctypes.c_int
+    L.lh_prefill_noalloc.argtypes = [vp, vp, vp, vp, i64, i64, i64, i64, ctypes.c_int, vp, vp, vp]
+    L.lh_prefill_noalloc.restype = ctypes.c_int
     L.lh_prefill_fft_workspace_bytes.argtypes = [i64, i64, i64, i64]
     L.lh_prefill_fft_workspace_bytes.restype = sz
     L.lh_prefill_fft.argtypes = [vp, vp, vp, vp, i64, i64, i64, i64, ctypes.c_int, vp, vp, vp, sz,
@@ -251,6 +257,17 @@ def prefill_with_plan(lam, R, h0, u, state, y, plan: int, workspace=None, stream
     _check(lib().lh_prefill_with_plan(lam.data_ptr(), R.data_ptr(), h0.data_ptr(), u.data_ptr(), B,
                                       D, d, T, io, state.data_ptr(), y.data_ptr(), plan, ws_ptr,
                                       ws_len, handle))
+
+
+def prefill_noalloc(lam, R, h0, u, state, y, stream=None) -> None:
+    """``prefill`` without a workspace (``lh_prefill_noalloc``): the library's
+    static per-GPU scratch serves the plan, so nothing is allocated.  Sizes
+    needing more than ``NOALLOC_SCRATCH_BYTES`` of scratch raise; calls that
+    overlap on one GPU race on that scratch."""
+    B, D, d, T, io = _prefill_args(lam, R, h0, u, state, y)
+    _check(lib().lh_prefill_noalloc(lam.data_ptr(), R.data_ptr(), h0.data_ptr(), u.data_ptr(), B,
+                                    D, d, T, io, state.data_ptr(), y.data_ptr(),
+                                    _stream(u.device, stream)[1]))
 
 
 def fft_workspace_bytes(B: int, D: int, d: int, T: int) -> int:

@@ -9,6 +9,8 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <mutex>
+
 #include "lh_internal.hpp"
 #include "prefill_fft.hpp"
 #include "companion.hpp"
@@ -148,7 +150,9 @@ lh_status check_prefill_buffers(const lh_c32* lambda, const lh_c32* R, const flo
     const Buf b_u = buf("u", u, T > 0 ? es * n_io : 0);
     const Buf b_state = buf("state", state, sizeof(lh_c32) * B * D * d);
     const Buf b_y = buf("y", y, T > 0 ? es * n_io : 0);
-    const Buf b_ws = buf("workspace", workspace, ws_needed);
+    // workspace == nullptr with ws_needed > 0 is reported below; the
+    // library's own scratch is passed as nullptr, 0, 0 and not checked here
+    const Buf b_ws = buf("workspace", workspace, workspace ? ws_needed : 0);
 
     if ((s = check_align(b_lam, 8)) || (s = check_align(b_R, 8)) || (s = check_align(b_h0, 4)) ||
         (s = check_align(b_state, 8)) || (s = check_align(b_u, es)) || (s = check_align(b_y, es)))
@@ -177,6 +181,44 @@ lh_status check_prefill_buffers(const lh_c32* lambda, const lh_c32* R, const flo
     const Buf* all[] = {&b_lam, &b_R, &b_h0, &b_u, &b_state, &b_y, &b_ws};
     for (const Buf* b : all)
         if ((s = check_accessible(*b, dev)) != LH_OK) return s;
+    return LH_OK;
+}
+
+// ---- static scratch of lh_prefill_noalloc
+//
+// Device memory that the library itself holds: one array per GPU the
+// library runs on, from the code object's load until the process ends.  In
+// host code `scratch` names a host-side stand-in, not the device array, so
+// it is never passed to a kernel or a copy: the device address comes from
+// hipGetSymbolAddress, resolved once per device (with that device current)
+// and kept in g_scratch_ptr.
+constexpr size_t kScratchBytes = size_t(LH_NOALLOC_SCRATCH_BYTES);
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mutex;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// The device address of this device's scratch array (resolved on first use).
+lh_status scratch_of(int dev, void** out)
+{
+    if (dev < 0 || dev >= kMaxDevices)
+        return fail(LH_ERR_NO_DEVICE, "device %d is beyond the %d devices the static scratch serves",
+                    dev, kMaxDevices);
+    std::lock_guard<std::mutex> lock(g_scratch_mutex);
+    if (g_scratch_ptr[dev] == nullptr) {
+        void* ptr = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || ptr == nullptr) {
+            (void)hipGetLastError();
+            return fail(LH_ERR_HIP, "hipGetSymbolAddress of the static scratch: %s",
+                        hipGetErrorString(e));
+        }
+        if (reinterpret_cast<uintptr_t>(ptr) % 256 != 0)
+            return fail(LH_ERR_HIP, "the static scratch is not 256-byte aligned");
+        g_scratch_ptr[dev] = ptr;
+    }
+    *out = g_scratch_ptr[dev];
     return LH_OK;
 }
 
@@ -274,6 +316,40 @@ lh_status lh_prefill(const lh_c32* lambda, const lh_c32* R, const float* h0, con
 {
     return lh_prefill_with_plan(lambda, R, h0, u, B, D, d, T, io_dtype, state, y,
                                 LH_PREFILL_AUTO, workspace, workspace_bytes, stream);
+}
+
+lh_status lh_prefill_noalloc(const lh_c32* lambda, const lh_c32* R, const float* h0,
+                             const void* u, int64_t B, int64_t D, int64_t d, int64_t T,
+                             lh_dtype io_dtype, lh_c32* state, void* y, void* stream)
+{
+    g_last_error[0] = '\0';
+    lh_status s;
+    if (!lambda || !R || !h0 || !state)
+        return fail(LH_ERR_INVALID_ARG, "lambda, R, h0 and state must not be NULL");
+    if ((s = check_sizes(B, D, d, T)) != LH_OK) return s;
+    if (T > 0 && (!u || !y)) return fail(LH_ERR_INVALID_ARG, "u and y must not be NULL when T > 0");
+    if ((s = check_dtype(io_dtype)) != LH_OK) return s;
+    lh::PrefillPlan pl;
+    if (!lh::make_prefill_plan(B, D, d, T, LH_PREFILL_AUTO, io_dtype == LH_BF16 ? 1 : 0, &pl))
+        return fail(LH_ERR_INVALID_ARG, "no prefill plan for these sizes");
+    if (pl.ws_bytes > kScratchBytes)
+        return fail(LH_ERR_WORKSPACE,
+                    "these sizes need %zu bytes of scratch; the static scratch of "
+                    "lh_prefill_noalloc holds %zu (call lh_prefill with a workspace)",
+                    pl.ws_bytes, kScratchBytes);
+    if ((s = check_prefill_buffers(lambda, R, h0, u, B, D, d, T, io_dtype, state, y, nullptr, 0,
+                                   0)) != LH_OK)
+        return s;
+    int dev = 0;
+    if ((s = check_device(&dev)) != LH_OK) return s;
+    void* ws = nullptr;
+    if (pl.ws_bytes > 0 && (s = scratch_of(dev, &ws)) != LH_OK) return s;
+    return from_hip(
+        lh::launch_prefill(reinterpret_cast<const float2*>(lambda),
+                           reinterpret_cast<const float2*>(R), h0, u, io_dtype == LH_BF16, B, D,
+                           d, T, reinterpret_cast<float2*>(state), y, pl, ws,
+                           static_cast<hipStream_t>(stream)),
+        "prefill launch");
 }
 
 size_t lh_prefill_fft_workspace_bytes(int64_t B, int64_t D, int64_t d, int64_t T)

@@ -447,3 +447,27 @@ def test_companion_workspace_and_no_device():
     assert L.lh_companion_step(*comp_step_args()) == 4
     assert L.lh_companion_init(*comp_init_args()) == 4
     assert L.lh_companion_init(*comp_init_args(T=0, u=None, ws=None, ws_bytes=0)) == 4
+
+
+def test_noalloc_rejects_sizes_beyond_its_scratch_before_any_device_work():
+    """lh_prefill_noalloc: a plan needing more than LH_NOALLOC_SCRATCH_BYTES of
+    scratch is refused on the host (LH_ERR_WORKSPACE), before the device is
+    touched; sizes within it reach the device check."""
+    L = lh.lib()
+    args = auto_args()
+    noalloc = args[:11] + [args[-1]]  # no workspace arguments
+    big = dict(B=256, D=2048, d=64, T=1024)  # float32 matrix-core tables: 75.5 MB
+    assert lh.workspace_bytes(256, 2048, 64, 1024) > lh.NOALLOC_SCRATCH_BYTES
+    a = auto_args(**big)
+    assert L.lh_prefill_noalloc(*(a[:11] + [a[-1]])) == 5
+    assert "scratch" in L.lh_last_error().decode()
+    assert L.lh_prefill_noalloc(*(auto_args(d=0)[:11] + [None])) == 1
+    if no_gpu():
+        assert L.lh_prefill_noalloc(*noalloc) == 4
+    assert header_enum_u64("LH_NOALLOC_SCRATCH_BYTES") == lh.NOALLOC_SCRATCH_BYTES
+
+
+def header_enum_u64(name):
+    text = open(HEADER).read()
+    m = re.search(r"#define\s+" + name + r"\s+\(UINT64_C\((\d+)\)\s*<<\s*(\d+)\)", text)
+    return int(m.group(1)) << int(m.group(2))
