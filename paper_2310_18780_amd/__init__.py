@@ -93,6 +93,12 @@ def lib() -> ctypes.CDLL:
         raise ImportError(
             f"{_LIB_PATH} is missing: build it with `python -m paper_2310_18780_amd.build` "
             "(or __graft_entry__.build()); there is no fallback implementation")
+    # torch first: it brings its own HIP runtime, and the library's dependency
+    # on the HIP runtime then resolves to that same, already loaded copy.
+    # Loaded the other way round, the process would hold two HIP runtimes and
+    # torch's memory and streams would be unknown to the library's.
+    import torch  # noqa: F401
+
     L = ctypes.CDLL(_LIB_PATH)
     i64, vp, sz = ctypes.c_int64, ctypes.c_void_p, ctypes.c_size_t
     L.lh_abi_version.argtypes = []

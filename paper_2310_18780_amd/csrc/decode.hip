@@ -12,10 +12,15 @@
 // d/2 mode pairs of a (b, c) row sit on LPR = d/2 consecutive lanes, one
 // 16-byte access each, so a wavefront reads and writes one contiguous span
 // of the state; the row sum is a butterfly over those lanes (DPP within 16
-// lanes).  Each thread serves NB = 8 batch rows of the same (c, mode pair):
-// lambda and R are loaded once for the eight rows, and every thread has
-// eight independent 16-byte state loads in flight before it computes.  A
-// workgroup is one wavefront (64 / LPR channels x 8 batch rows).
+// lanes).  Each thread serves NB batch rows of the same (c, mode pair):
+// lambda and R are loaded once for the NB rows, and every thread has NB
+// independent 16-byte state loads in flight before it computes.  NB = 8
+// where that still gives 2048 wavefronts (two per SIMD), else 4 where that
+// does, else 2: small states are latency-bound, and more wavefronts with
+// fewer rows each finish sooner (B = 16, D = 768, d = 16: 1.95 us per step
+// with NB = 2 against 2.51 us with NB = 8; B = 64, D = 2048: 6.0 us with
+// NB = 8 against 6.3 us with NB = 4).  A workgroup is one wavefront
+// (64 / LPR channels x NB batch rows).
 //
 // Cache policy: the state is written with the non-temporal hint, and read
 // with it when the whole state fits the L2s (at most kStreamStateBytes, 32
@@ -46,7 +51,8 @@ namespace {
 constexpr int kBlock = 256;      // generic path
 constexpr int kPairsBlock = 64;  // fast path: one wavefront per workgroup
 constexpr int kXcds = 8;
-constexpr int kRowsPerThread = 8;
+constexpr int kMaxRowsPerThread = 8;
+constexpr int64_t kMinWaves = 2048;  // wavefronts the row count per thread is chosen for
 constexpr int64_t kStreamStateBytes = INT64_C(32) << 20;  // non-temporal state loads up to this size
 
 typedef float f4v __attribute__((ext_vector_type(4)));
@@ -134,13 +140,12 @@ __device__ __forceinline__ float re_dot_pair(float4 r, float4 x)
 // to a multiple of 8; workgroup x runs on XCD x % 8, which owns tiles
 // [(x % 8) T8, (x % 8 + 1) T8) with T8 = gridDim.x / 8.  NTL: non-temporal
 // state loads.
-template <typename IO, int LPR, bool NTL>
+template <typename IO, int LPR, bool NTL, int NB>
 __global__ __launch_bounds__(kPairsBlock) void step_pairs_kernel(
     const float2* __restrict__ lam, const float2* __restrict__ R, const float* __restrict__ h0,
     float2* __restrict__ state, const IO* __restrict__ u, IO* __restrict__ y, int B, int D,
     int ntiles)
 {
-    constexpr int NB = kRowsPerThread;
     constexpr int kRows = kPairsBlock / LPR;  // channels per workgroup
     constexpr int d = 2 * LPR;
     const int ct = int(blockIdx.x % kXcds) * int(gridDim.x / kXcds) + int(blockIdx.x / kXcds);
@@ -230,12 +235,21 @@ __global__ __launch_bounds__(kBlock) void step_generic_kernel(
     if (valid && j == 0) io_store(y + b * D + c, fmaf(h0[c], uv, acc));
 }
 
+// Batch rows per thread of the fast path (see the file comment).
+int pairs_rows_per_thread(int lpr, int64_t B, int64_t D)
+{
+    const int64_t waves_per_group = (D * lpr + 63) / 64;
+    for (int nb = kMaxRowsPerThread; nb > 2; nb /= 2)
+        if ((B + nb - 1) / nb * waves_per_group >= kMinWaves) return nb;
+    return 2;
+}
+
 // 2-D grid of the fast path; false when it does not fit the grid limits
-bool pairs_grid(int lpr, int64_t B, int64_t D, dim3* g, int* ntiles)
+bool pairs_grid(int lpr, int nb, int64_t B, int64_t D, dim3* g, int* ntiles)
 {
     const int64_t rows_per_block = kPairsBlock / lpr;
     const int64_t nt = (D + rows_per_block - 1) / rows_per_block;
-    const int64_t nbg = (B + kRowsPerThread - 1) / kRowsPerThread;
+    const int64_t nbg = (B + nb - 1) / nb;
     const int64_t ntp = (nt + kXcds - 1) / kXcds * kXcds;
     if (ntp > 0x7fffffff || nbg > 65535) return false;
     *g = dim3(uint32_t(ntp), uint32_t(nbg));
@@ -243,7 +257,7 @@ bool pairs_grid(int lpr, int64_t B, int64_t D, dim3* g, int* ntiles)
     return true;
 }
 
-template <typename IO, bool NTL>
+template <typename IO, bool NTL, int NB>
 hipError_t launch_pairs(int lpr, dim3 grid, int ntiles, const float2* lam, const float2* R,
                         const float* h0, float2* state, const void* u, void* y, int64_t B,
                         int64_t D, hipStream_t stream)
@@ -251,10 +265,10 @@ hipError_t launch_pairs(int lpr, dim3 grid, int ntiles, const float2* lam, const
     const IO* uu = static_cast<const IO*>(u);
     IO* yy = static_cast<IO*>(y);
     const int b = int(B), dd = int(D);
-#define LH_PAIRS(L)                                                                           \
-    case L:                                                                                   \
-        hipLaunchKernelGGL((step_pairs_kernel<IO, L, NTL>), grid, dim3(kPairsBlock), 0, stream, \
-                           lam, R, h0, state, uu, yy, b, dd, ntiles);                         \
+#define LH_PAIRS(L)                                                                          \
+    case L:                                                                                  \
+        hipLaunchKernelGGL((step_pairs_kernel<IO, L, NTL, NB>), grid, dim3(kPairsBlock), 0,  \
+                           stream, lam, R, h0, state, uu, yy, b, dd, ntiles);                \
         break;
     switch (lpr) {
         LH_PAIRS(1)
@@ -269,6 +283,23 @@ hipError_t launch_pairs(int lpr, dim3 grid, int ntiles, const float2* lam, const
     }
 #undef LH_PAIRS
     return hipGetLastError();
+}
+
+template <typename IO, bool NTL>
+hipError_t launch_pairs_nb(int nb, int lpr, dim3 grid, int ntiles, const float2* lam,
+                           const float2* R, const float* h0, float2* state, const void* u, void* y,
+                           int64_t B, int64_t D, hipStream_t stream)
+{
+    switch (nb) {
+        case 8:
+            return launch_pairs<IO, NTL, 8>(lpr, grid, ntiles, lam, R, h0, state, u, y, B, D, stream);
+        case 4:
+            return launch_pairs<IO, NTL, 4>(lpr, grid, ntiles, lam, R, h0, state, u, y, B, D, stream);
+        case 2:
+            return launch_pairs<IO, NTL, 2>(lpr, grid, ntiles, lam, R, h0, state, u, y, B, D, stream);
+        default:
+            return hipErrorInvalidValue;
+    }
 }
 
 template <typename IO, int VEC>
@@ -314,18 +345,19 @@ hipError_t launch_step(const float2* lam, const float2* R, const float* h0, floa
     dim3 grid;
     int ntiles = 0;
     const int fast_lpr = static_cast<int>(pairs);
+    const int nb = pow2_pairs ? pairs_rows_per_thread(fast_lpr, B, D) : 2;
     if (pow2_pairs && aligned16 && B < (INT64_C(1) << 31) && D < (INT64_C(1) << 31) &&
-        pairs_grid(fast_lpr, B, D, &grid, &ntiles)) {
+        pairs_grid(fast_lpr, nb, B, D, &grid, &ntiles)) {
         const bool ntl = 8 * B * D * d <= kStreamStateBytes;
         if (bf16_io)
-            return ntl ? launch_pairs<bf16, true>(fast_lpr, grid, ntiles, lam, R, h0, state, u_t,
-                                                  y_t, B, D, stream)
-                       : launch_pairs<bf16, false>(fast_lpr, grid, ntiles, lam, R, h0, state, u_t,
-                                                   y_t, B, D, stream);
-        return ntl ? launch_pairs<float, true>(fast_lpr, grid, ntiles, lam, R, h0, state, u_t, y_t,
-                                               B, D, stream)
-                   : launch_pairs<float, false>(fast_lpr, grid, ntiles, lam, R, h0, state, u_t,
-                                                y_t, B, D, stream);
+            return ntl ? launch_pairs_nb<bf16, true>(nb, fast_lpr, grid, ntiles, lam, R, h0,
+                                                     state, u_t, y_t, B, D, stream)
+                       : launch_pairs_nb<bf16, false>(nb, fast_lpr, grid, ntiles, lam, R, h0,
+                                                      state, u_t, y_t, B, D, stream);
+        return ntl ? launch_pairs_nb<float, true>(nb, fast_lpr, grid, ntiles, lam, R, h0, state,
+                                                  u_t, y_t, B, D, stream)
+                   : launch_pairs_nb<float, false>(nb, fast_lpr, grid, ntiles, lam, R, h0, state,
+                                                   u_t, y_t, B, D, stream);
     }
     // generic layouts
     int lpr = 1;

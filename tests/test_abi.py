@@ -471,3 +471,19 @@ def header_enum_u64(name):
     text = open(HEADER).read()
     m = re.search(r"#define\s+" + name + r"\s+\(UINT64_C\((\d+)\)\s*<<\s*(\d+)\)", text)
     return int(m.group(1)) << int(m.group(2))
+
+
+def test_one_hip_runtime_whatever_the_import_order():
+    """Loading the library before anything imported torch must still leave
+    one HIP runtime in the process (torch's), so that torch's memory and
+    streams are the library's too."""
+    import subprocess
+    import sys
+
+    code = ("import paper_2310_18780_amd as lh; lh.lib(); import torch; "
+            "maps = open('/proc/self/maps').read(); "
+            "print(len({l.split()[-1] for l in maps.splitlines() if 'libamdhip64' in l}))")
+    out = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True,
+                         timeout=120, cwd=ROOT)
+    assert out.returncode == 0, out.stderr
+    assert out.stdout.strip() == "1", out.stdout
