@@ -23,18 +23,19 @@
 // (64 / LPR channels x NB batch rows).
 //
 // Cache policy: the state is written with the non-temporal hint, and read
-// with it when the whole state fits the L2s (at most kStreamStateBytes, 32
-// MiB across the 8 XCDs).  An in-place pass that reads its lines with
-// ordinary loads leaves them in the caches to be written back later; a state
-// streaming from HBM (as the states of a model's layers together do) then
-// runs about a quarter slower than a copy of the same bytes, and with
-// non-temporal loads at the copy's rate.  A state that fits the L2s and is
-// stepped again right away stays there either way (within 1%).  A larger
-// state stepped again right away keeps part of itself in the 256 MB Infinity
-// Cache only when read with ordinary loads (a 256 MiB state: 76 us per step
-// against 87 us), so those take ordinary loads.  y_t is stored with ordinary
-// stores: its 16-byte pieces per wavefront and batch row are merged into
-// whole lines in the L2 before they reach HBM.
+// with it when the whole state fits the L2s with room to spare (at most
+// kStreamStateBytes, 16 MiB: half of the 8 XCDs' 4 MB L2s).  An in-place
+// pass that reads its lines with ordinary loads leaves them in the caches to
+// be written back later; a state streaming from HBM (as the states of a
+// model's layers together do) then runs about a quarter slower than a copy
+// of the same bytes, and with non-temporal loads at the copy's rate.  A
+// state that fits the L2s and is stepped again right away stays there either
+// way (16 MiB: within 1%).  A larger state stepped again right away keeps
+// part of itself in the 256 MB Infinity Cache only when read with ordinary
+// loads (32 MiB: 11.0 us per step against 11.8 us; 256 MiB: 76 us against
+// 87 us), so those take ordinary loads.  y_t is stored with ordinary stores:
+// its 16-byte pieces per wavefront and batch row are merged into whole lines
+// in the L2 before they reach HBM.
 //
 // Workgroups are ordered so that XCD x (workgroup i runs on XCD i mod 8)
 // owns one contiguous range of channel tiles: its lambda / R rows, its slice
@@ -53,7 +54,7 @@ constexpr int kPairsBlock = 64;  // fast path: one wavefront per workgroup
 constexpr int kXcds = 8;
 constexpr int kMaxRowsPerThread = 8;
 constexpr int64_t kMinWaves = 2048;  // wavefronts the row count per thread is chosen for
-constexpr int64_t kStreamStateBytes = INT64_C(32) << 20;  // non-temporal state loads up to this size
+constexpr int64_t kStreamStateBytes = INT64_C(16) << 20;  // non-temporal state loads up to this size
 
 typedef float f4v __attribute__((ext_vector_type(4)));
 

@@ -63,7 +63,7 @@ def inputs(B, D, d, T, K, io, seed=0, r=(0.5, 0.999)):
     return to_device(lam, R, h0, up, ud, io)
 
 
-@pytest.mark.parametrize("kind", ["segmented", "fft"])
+@pytest.mark.parametrize("kind", ["segmented", "fft", "noalloc"])
 def test_prefill_plans(kind):
     import torch
 
@@ -80,11 +80,16 @@ def test_prefill_plans(kind):
 
         def run():
             lh.prefill(t["lam"], t["R"], t["h0"], t["u"], state, y, workspace=ws)
-    else:
+    elif kind == "fft":
         ws = torch.empty(lh.fft_workspace_bytes(B, D, d, T), dtype=torch.uint8, device="cuda")
 
         def run():
             lh.prefill_fft(t["lam"], t["R"], t["h0"], t["u"], state, y, workspace=ws)
+    else:  # the segmented plan on the library's static scratch: nothing allocated
+        assert 0 < lh.workspace_bytes(B, D, d, T) <= lh.NOALLOC_SCRATCH_BYTES
+
+        def run():
+            lh.prefill_noalloc(t["lam"], t["R"], t["h0"], t["u"], state, y)
 
     def reset():
         y.fill_(float("nan"))
