@@ -20,7 +20,10 @@
 // fewer rows each finish sooner (B = 16, D = 768, d = 16: 1.95 us per step
 // with NB = 2 against 2.51 us with NB = 8; B = 64, D = 2048: 6.0 us with
 // NB = 8 against 6.3 us with NB = 4).  A workgroup is one wavefront
-// (64 / LPR channels x NB batch rows).
+// (64 / LPR channels x NB batch rows) up to LPR = 16; with LPR >= 32 (d >=
+// 64, two channels or fewer per wavefront) it is four wavefronts, so that
+// a workgroup covers 8 channels (B = 256, D = 2048, d = 64: 71 us per step
+// against 76 us with one-wavefront workgroups).
 //
 // Cache policy: the state is written with the non-temporal hint, and read
 // with it when the whole state fits the L2s with room to spare (at most
@@ -49,8 +52,10 @@
 namespace lh {
 namespace {
 
-constexpr int kBlock = 256;      // generic path
-constexpr int kPairsBlock = 64;  // fast path: one wavefront per workgroup
+constexpr int kBlock = 256;  // generic path
+
+// fast path: threads per workgroup for LPR lanes per row
+constexpr int pairs_block(int lpr) { return lpr >= 32 ? 256 : 64; }
 constexpr int kXcds = 8;
 constexpr int kMaxRowsPerThread = 8;
 constexpr int64_t kMinWaves = 2048;  // wavefronts the row count per thread is chosen for
@@ -142,12 +147,12 @@ __device__ __forceinline__ float re_dot_pair(float4 r, float4 x)
 // [(x % 8) T8, (x % 8 + 1) T8) with T8 = gridDim.x / 8.  NTL: non-temporal
 // state loads.
 template <typename IO, int LPR, bool NTL, int NB>
-__global__ __launch_bounds__(kPairsBlock) void step_pairs_kernel(
+__global__ __launch_bounds__(pairs_block(LPR)) void step_pairs_kernel(
     const float2* __restrict__ lam, const float2* __restrict__ R, const float* __restrict__ h0,
     float2* __restrict__ state, const IO* __restrict__ u, IO* __restrict__ y, int B, int D,
     int ntiles)
 {
-    constexpr int kRows = kPairsBlock / LPR;  // channels per workgroup
+    constexpr int kRows = pairs_block(LPR) / LPR;  // channels per workgroup
     constexpr int d = 2 * LPR;
     const int ct = int(blockIdx.x % kXcds) * int(gridDim.x / kXcds) + int(blockIdx.x / kXcds);
     const int b0 = blockIdx.y * NB;
@@ -248,7 +253,7 @@ int pairs_rows_per_thread(int lpr, int64_t B, int64_t D)
 // 2-D grid of the fast path; false when it does not fit the grid limits
 bool pairs_grid(int lpr, int nb, int64_t B, int64_t D, dim3* g, int* ntiles)
 {
-    const int64_t rows_per_block = kPairsBlock / lpr;
+    const int64_t rows_per_block = pairs_block(lpr) / lpr;
     const int64_t nt = (D + rows_per_block - 1) / rows_per_block;
     const int64_t nbg = (B + nb - 1) / nb;
     const int64_t ntp = (nt + kXcds - 1) / kXcds * kXcds;
@@ -268,7 +273,7 @@ hipError_t launch_pairs(int lpr, dim3 grid, int ntiles, const float2* lam, const
     const int b = int(B), dd = int(D);
 #define LH_PAIRS(L)                                                                          \
     case L:                                                                                  \
-        hipLaunchKernelGGL((step_pairs_kernel<IO, L, NTL, NB>), grid, dim3(kPairsBlock), 0,  \
+        hipLaunchKernelGGL((step_pairs_kernel<IO, L, NTL, NB>), grid, dim3(pairs_block(L)), 0, \
                            stream, lam, R, h0, state, uu, yy, b, dd, ntiles);                \
         break;
     switch (lpr) {
