@@ -31,7 +31,7 @@ if ROOT not in sys.path:
 METRIC = "decode tokens/s (B·steps/s) + HBM GB/s at D=2048,d=16; prefill tokens/s"
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E
 FP32_VALU_PEAK_TFLOPS = 157.3  # MI355X fp32 vector (with packed FP32 FMA)
-FP32_MFMA_PEAK_TFLOPS = 157.3  # MI355X dense fp32 matrix
+BF16_MFMA_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 matrix (no sparsity)
 PROFILES = os.path.join(ROOT, "profiles")
 
 
@@ -144,14 +144,16 @@ def prefill_flops(w):
     return 12 * w.d * w.B * w.T * w.D + 2 * w.B * w.T * w.D
 
 
-def mfma32_flops(w):
-    """Flops of the float32 matrix-core plan at d = 64 (16x16x4 products, 2048
-    flops each): per channel, 16-row column block and 32-step chunk, 64
-    products for the chunk's end state (P U), 16 for the outputs from the
-    chunk's inputs (T U) and 64 for those from its entry state (W X); a
-    partial last chunk takes the 80 output products only."""
+def mfma64_flops(w):
+    """Flops the d = 64 matrix-core plan executes (16x16x32 bfloat16
+    products, 16384 flops each; float32 operands in three bfloat16 terms, six
+    term products per contraction): per channel, 16-row column block and
+    32-step chunk, 48 products for the chunk's end state (8 row tiles of P U),
+    12 for the outputs from the chunk's inputs (2 row tiles of T U) and 32 for
+    those from its entry state (W X: 2 row tiles x 4 K tiles x 4 term
+    products); a partial last chunk takes the 44 output products only."""
     full, part = w.T // 32, int(w.T % 32 != 0)
-    return 2048 * w.D * -(-w.B // 16) * (144 * full + 80 * part)
+    return 16384 * w.D * -(-w.B // 16) * (92 * full + 44 * part)
 
 
 def dtype_detail(w, plan):
@@ -160,8 +162,6 @@ def dtype_detail(w, plan):
         else "float32 u/y"
     if plan == "scan":
         pre = "prefill on the float32 VALU"
-    elif w.d == 64:
-        pre = "prefill contractions on float32 matrix cores (16x16x4 f32)"
     elif w.io == "bf16":
         pre = ("prefill contractions on bfloat16 matrix cores with float32 accumulation: "
                "float32 operands split into bfloat16 terms, two for the outputs, three for "
@@ -892,22 +892,23 @@ def main():
                               src_digest("decode.hip", "lh_internal.hpp"))
     pre_digest = src_digest("prefill.hip", "prefill_mfma.hip", "lh_internal.hpp")
     traffic_pre = counter_traffic(f"prefill_{w.name}_counters.txt", pre_digest)
-    # The bfloat16-operand matrix-core plans (d = 16, 32) execute the
-    # contractions on the MFMA units far below the MFMA ridge, so their
-    # roofline is HBM; the float32-operand plan of d = 64 issues 144 16x16x4
-    # products per channel, 16 rows and 32 steps and is bound by the fp32
-    # MFMA rate; the VALU scan executes about the declared flops at high
+    # The matrix-core plans at d = 16 and 32 execute their split-term
+    # contractions far below the bfloat16 MFMA ridge (at most 208 flops per
+    # byte of u and y against 2500 / 8 = 312), so their roofline is HBM; at
+    # d = 64 the 92 products per channel, 16 rows and 32 steps come to 368
+    # flops per byte, above the ridge, so its roofline is the bfloat16 MFMA
+    # peak; the VALU scan executes about the declared flops at high
     # intensity, so its roofline is the VALU peak.
     plan = lh.prefill_plan(w.B, w.D, w.d, w.T, io=w.io)
     pre_gbs = prefill_bytes(w) / (pre_avg * 1e-3) / 1e9
     if plan == "scan":
         roofline_prefill = {"bound": "alu", "achieved": pre_tf, "peak": FP32_VALU_PEAK_TFLOPS,
                             "unit": "TFLOP/s", "frac": pre_tf / FP32_VALU_PEAK_TFLOPS}
-    elif w.d == 64:  # float32 matrix-core plan: bound by the fp32 MFMA rate
-        mf = mfma32_flops(w) / (pre_avg * 1e-3) / 1e12
-        roofline_prefill = {"bound": "mfma", "achieved": mf, "peak": FP32_MFMA_PEAK_TFLOPS,
-                            "unit": "TFLOP/s", "frac": mf / FP32_MFMA_PEAK_TFLOPS,
-                            "mfma_flops_per_launch": mfma32_flops(w),
+    elif w.d == 64:  # matrix-core plan above the MFMA ridge: bound by the bf16 MFMA rate
+        mf = mfma64_flops(w) / (pre_avg * 1e-3) / 1e12
+        roofline_prefill = {"bound": "mfma", "achieved": mf, "peak": BF16_MFMA_PEAK_TFLOPS,
+                            "unit": "TFLOP/s", "frac": mf / BF16_MFMA_PEAK_TFLOPS,
+                            "mfma_flops_per_launch": mfma64_flops(w),
                             "hbm_frac": pre_gbs / HBM_PEAK_GBS}
     else:
         roofline_prefill = {"bound": "hbm", "achieved": pre_gbs, "peak": HBM_PEAK_GBS,

@@ -195,11 +195,10 @@ size_t lh_prefill_with_plan_workspace_bytes(int64_t B, int64_t D, int64_t d, int
  *   plan = LH_PREFILL_MFMA: the matrix-core plan (chunks of 32 steps as dense
  *            contractions on the MFMA units: outputs Y = T U + W X_in, chunk
  *            end states S = P U and the carry X_in <- lambda^32 X_in + S; with
- *            d = 16 or 32 the float32 operands are split into bfloat16 terms,
- *            three with float32 u/y, two for the outputs and three for the
- *            state with bfloat16 u/y, and D % 8 == 0 is required; with d = 64
- *            the operands stay float32 (16x16x4 float32 products), u/y must be
- *            float32 and D % 4 == 0; always T >= 1 and 16-byte aligned u and
+ *            the float32 operands split into bfloat16 terms: three with
+ *            float32 u/y, two for the outputs and three for the state with
+ *            bfloat16 u/y; d = 16 or 32 require D % 8 == 0, d = 64 requires
+ *            float32 u/y and D % 4 == 0; always T >= 1 and 16-byte aligned u and
  *            y, else LH_ERR_INVALID_ARG).  The automatic plan uses it where
  *            supported and either ceil(D/16) * ceil(B/32) >= 256 (enough
  *            workgroups to fill the GPU without splitting the prompt in time)

@@ -33,16 +33,16 @@
 // split by the setup kernel into the workspace, already in the lane order of
 // the A operand.
 //
-// d = 64 (float32 u/y only) runs on v_mfma_f32_16x16x4_f32 without splitting:
-// the same three contractions as 144 products of K = 4 per channel, chunk and
-// 16 rows (64 for S, 16 for T U, 64 for W X_in), in float32 throughout.  Its
-// 144 operand values per lane and channel fill most of a SIMD's 512
-// registers, so its workgroups have 4 waves (one per SIMD, 4 channels) and
-// each wave takes two groups of 16 rows.
+// d = 64 (float32 u/y only) takes the same three-term operands: 18 A
+// fragments per channel (216 registers per lane), which with the states and
+// accumulators need more than the 256 registers of two waves per SIMD, so its
+// workgroups have 4 waves (one per SIMD, up to 512 registers: the compiler
+// keeps the accumulators in the accumulation registers), one channel and 16
+// rows each.
 //
 // Work layout: a wavefront owns CPW channels (2 for bfloat16 inputs with
 // d = 16, else 1) and NBG groups of 16 batch rows (2 for float32 inputs with
-// d = 16 or 64 and more than 16 rows, else 1), and walks all chunks of the
+// d = 16 and more than 16 rows, else 1), and walks all chunks of the
 // prompt, keeping its matrices (A operands) and the carried states in
 // registers.  With the 16x16 accumulator layout (lane n + 16 g holds rows
 // 4g..4g+3 of column n) and state rows ordered [Re modes | Im modes], the
@@ -81,17 +81,9 @@ constexpr int kMinWorkgroups = 256;  // automatic plan: at least one workgroup p
 // A-operand fragments per channel: P (2d/16 tiles), T (2 tiles), W (2 tiles x d/16 K-steps)
 __host__ __device__ constexpr int n_frag(int DM) { return 2 * DM + 2 + 2 * DM; }
 
-// d = 64 (DM = 4) runs on v_mfma_f32_16x16x4_f32 instead: float32 operands,
-// one float per lane per 16 x 4 block (lane l holds A[l % 16][l / 16] and
-// B[l / 16][l % 16]), no splitting, K = 4 per instruction.  A-operand blocks
-// per channel: P 2 DM row tiles x 8 K-steps, T 2 x 8, W 2 x 2 DM x 4.  The
-// three-term bfloat16 operands of 64 modes would not fit the registers.
-__host__ __device__ constexpr int n_frag32(int DM) { return 16 * DM + 16 + 16 * DM; }
-
 size_t frag_bytes_of(int64_t D, int DM)
 {
-    return DM == 4 ? size_t(D) * n_frag32(DM) * 64 * sizeof(float)
-                   : size_t(D) * n_frag(DM) * kTerms * 64 * sizeof(bf16x8);
+    return size_t(D) * n_frag(DM) * kTerms * 64 * sizeof(bf16x8);
 }
 
 __device__ __forceinline__ void split3(float v, __bf16& a, __bf16& b, __bf16& c)
@@ -127,11 +119,6 @@ __device__ __forceinline__ f32x4 mfma(bf16x8 a, bf16x8 b, f32x4 c)
     return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
 }
 
-__device__ __forceinline__ f32x4 mfma32(float a, float b, f32x4 c)
-{
-    return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
-}
-
 // Workgroup barrier that orders LDS only: waits for this wave's LDS accesses
 // (lgkmcnt(0); vmcnt and expcnt left at their maximum in the s_waitcnt
 // encoding) and leaves global loads in flight, unlike __syncthreads(), whose
@@ -160,7 +147,7 @@ __global__ __launch_bounds__(256) void mfma_setup_kernel(const float2* __restric
                                                          float2* __restrict__ lamc, int tw_terms)
 {
     constexpr int d = 16 * DM;
-    constexpr int F = DM == 4 ? n_frag32(DM) : n_frag(DM);
+    constexpr int F = n_frag(DM);
     __shared__ double pwr[d][kC + 1], pwi[d][kC + 1];
     __shared__ double taps[kC];
     const int c = blockIdx.x;
@@ -200,28 +187,6 @@ __global__ __launch_bounds__(256) void mfma_setup_kernel(const float2* __restric
         }
         const int f = item / 64, lane = item % 64;
         const int g = lane / 16, m = lane % 16;
-        if constexpr (DM == 4) {  // float32 blocks; K-step s of a chunk takes steps 8 g + s
-            double val;
-            if (f < 16 * DM) {  // P row tile q, K-step s: row 16 q + m, step 8 g + s
-                const int q = f / 8, s2 = f % 8;
-                const int r = 16 * q + m, j = 8 * g + s2;
-                val = r < d ? pwr[r][kC - 1 - j] : pwi[r - d][kC - 1 - j];
-            } else if (f < 16 * DM + 16) {  // T row tile mt, K-step s
-                const int mt = (f - 16 * DM) / 8, s2 = (f - 16 * DM) % 8;
-                const int t = 16 * mt + m, j = 8 * g + s2;
-                val = j <= t ? taps[t - j] : 0.0;
-            } else {  // W row tile mt, state tile q (Re q < DM, else Im), row i of the lane's 4
-                const int w = f - 16 * DM - 16;
-                const int mt = w / (8 * DM), q = (w % (8 * DM)) / 4, i = w % 4;
-                const int t = 16 * mt + m;
-                const int n = 16 * (q % DM) + 4 * g + i;
-                const double rr = rc[n].x, ri = rc[n].y;
-                val = q < DM ? rr * pwr[n][t] - ri * pwi[n][t]      // Re(R lambda^t)
-                             : -(rr * pwi[n][t] + ri * pwr[n][t]);  // -Im(R lambda^t)
-            }
-            reinterpret_cast<float*>(frag)[(int64_t(c) * F + f) * 64 + lane] = float(val);
-            continue;
-        }
         bf16x8 t0, t1, t2;
         for (int i = 0; i < 8; ++i) {
             const int k = 8 * g + i;  // K index of this element
@@ -286,9 +251,9 @@ template <>
 struct Tiling<float, 4> {
     static constexpr int CPW = 1;
 };
-// Waves per workgroup: 8 (two per SIMD) with bfloat16 operands; 4 with the
-// float32 operands of d = 64, whose 144 A values per lane and channel need
-// the whole register file of a SIMD (one wave each, up to 512 registers).
+// Waves per workgroup: 8 (two per SIMD); 4 at d = 64, whose 216 A-operand
+// registers per lane and channel need most of a SIMD's register file (one
+// wave each, up to 512 registers).
 __host__ __device__ constexpr int waves_of(int DM) { return DM == 4 ? 4 : 8; }
 
 // LDS element type of the staged u tile and operand term counts: bfloat16
@@ -355,10 +320,8 @@ __global__ __launch_bounds__(64 * waves_of(DM)) void mfma_prefill_kernel(
     int nseg, int64_t seg_len, float2* __restrict__ xs)
 {
     constexpr int d = 16 * DM;
-    constexpr bool k32 = DM == 4;                     // float32 operands (v_mfma_f32_16x16x4_f32)
-    static_assert(!k32 || sizeof(IO) == 4, "d = 64 takes float32 u and y");
-    constexpr int F = k32 ? 1 : n_frag(DM);
-    constexpr int F32 = k32 ? n_frag32(DM) : 1;
+    static_assert(DM < 4 || sizeof(IO) == 4, "d = 64 takes float32 u and y");
+    constexpr int F = n_frag(DM);
     constexpr int CPW = cpw_of<IO, DM, MODE>();
     constexpr int NW = waves_of(DM);
     constexpr int NT = 64 * NW;                       // threads
@@ -422,21 +385,14 @@ __global__ __launch_bounds__(64 * waves_of(DM)) void mfma_prefill_kernel(
     // ---- A operands and lambda^C of this wave's channels (clamped into range;
     // results of channels >= D are never stored)
     bf16x8 A[CPW][F][KTX];
-    float A32[CPW][F32];
 #pragma unroll
     for (int k = 0; k < CPW; ++k) {
         const int cc = min(c0 + w * CPW + k, D - 1);
-        if constexpr (k32) {
-            const float* fr = reinterpret_cast<const float*>(frag) + int64_t(cc) * F32 * 64 + lane;
 #pragma unroll
-            for (int f = 0; f < F32; ++f) A32[k][f] = fr[f * 64];
-        } else {
+        for (int f = 0; f < F; ++f)
 #pragma unroll
-            for (int f = 0; f < F; ++f)
-#pragma unroll
-                for (int s = 0; s < (f < 2 * DM ? KTP : KT); ++s)
-                    A[k][f][s] = frag[((int64_t(cc) * F + f) * kTerms + s) * 64 + lane];
-        }
+            for (int s = 0; s < (f < 2 * DM ? KTP : KT); ++s)
+                A[k][f][s] = frag[((int64_t(cc) * F + f) * kTerms + s) * 64 + lane];
         if (n < 4 * DM)  // lambda^C of the modes of lane group g (read back by the carry)
             lcs[w * CPW + k][g][n] = lamc[(int64_t(cc) * 4 + g) * (4 * DM) + n];
     }
@@ -558,51 +514,6 @@ __global__ __launch_bounds__(64 * waves_of(DM)) void mfma_prefill_kernel(
             }
         }
     };
-    // the same steps as float32 B operands, one per K-step of 16x16x4
-    auto load_u32 = [&](int k, int bg, float (&U)[8], const ST* ub) {
-        const int ue = ((w * CPW + k) * BN + kN * bg + n) * US + 8 * g;
-        const float4 lo = *reinterpret_cast<const float4*>(&ub[ue]);
-        const float4 hi = *reinterpret_cast<const float4*>(&ub[ue + 4]);
-        U[0] = lo.x, U[1] = lo.y, U[2] = lo.z, U[3] = lo.w;
-        U[4] = hi.x, U[5] = hi.y, U[6] = hi.z, U[7] = hi.w;
-    };
-    // float32 operands (d = 64), one channel k and batch group bg: outputs of
-    // the chunk from the entry state, Y = T U + W X_in (K-step (q, i) of W X_in
-    // takes row i of state tile q, which each lane already holds)
-    auto y32 = [&](int k, const float (&U)[8], const f32x4 (&Xs)[2 * DM], f32x4 (&Y)[2]) {
-        Y[0] = Y[1] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int s = 0; s < 8; ++s)
-#pragma unroll
-            for (int mt = 0; mt < 2; ++mt) Y[mt] = mfma32(A32[k][16 * DM + 8 * mt + s], U[s], Y[mt]);
-#pragma unroll
-        for (int q = 0; q < 2 * DM; ++q)
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-#pragma unroll
-                for (int mt = 0; mt < 2; ++mt)
-                    Y[mt] = mfma32(A32[k][16 * DM + 16 + 8 * DM * mt + 4 * q + i], Xs[q][i], Y[mt]);
-    };
-    // chunk end state from the chunk's inputs, S = P U, and the carry
-    // X <- lambda^C X + S, one state tile pair (Re q, Im q) at a time
-    auto carry32 = [&](int k, int bg, const float (&U)[8]) {
-#pragma unroll
-        for (int q = 0; q < DM; ++q) {
-            f32x4 Sr = f32x4{0.f, 0.f, 0.f, 0.f}, Si = Sr;
-#pragma unroll
-            for (int s = 0; s < 8; ++s) {
-                Sr = mfma32(A32[k][8 * q + s], U[s], Sr);
-                Si = mfma32(A32[k][8 * (DM + q) + s], U[s], Si);
-            }
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const float2 l = lcs[w * CPW + k][g][4 * q + i];
-                const float xr = X[k][bg][q][i], xi = X[k][bg][DM + q][i];
-                X[k][bg][q][i] = fmaf(l.x, xr, fmaf(-l.y, xi, Sr[i]));
-                X[k][bg][DM + q][i] = fmaf(l.x, xi, fmaf(l.y, xr, Si[i]));
-            }
-        }
-    };
     // X_in as the B operand of W X_in (K index 8g + i <-> tile q (i < 4),
     // tile DM + q (i >= 4)) in two bfloat16 terms: the correction W X_in then
     // carries a relative error near 2^-16 while the carried state itself
@@ -649,80 +560,65 @@ __global__ __launch_bounds__(64 * waves_of(DM)) void mfma_prefill_kernel(
     // for all independent accumulators of the wave's channels (2 Y tiles and
     // 2 DM S tiles per channel), then the carry and the output stage
     auto compute_full = [&](const ST* ub, uint32_t* ys) {
-        if constexpr (k32) {
 #pragma unroll
-            for (int bg = 0; bg < NBG; ++bg) {
-                f32x4 Y[CPW][2];
+        for (int bg = 0; bg < NBG; ++bg) {
+            bf16x8 U[CPW][NTU];
+            bf16x8 XB[CPW][DM][2];
+            f32x4 Y[CPW][2], Sr[CPW][DM], Si[CPW][DM];
 #pragma unroll
-                for (int k = 0; k < CPW; ++k) {
-                    float U[8];
-                    load_u32(k, bg, U, ub);
-                    if constexpr (MODE != kSegState) y32(k, U, X[k][bg], Y[k]);
-                    carry32(k, bg, U);
-                }
-                if constexpr (MODE != kSegState) stage_y(bg, Y, ys);
+            for (int k = 0; k < CPW; ++k) {
+                load_u(k, bg, U[k], ub);
+                if constexpr (MODE != kSegState) split_x(X[k][bg], XB[k]);
+                Y[k][0] = Y[k][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int q = 0; q < DM; ++q) Sr[k][q] = Si[k][q] = f32x4{0.f, 0.f, 0.f, 0.f};
             }
-        } else {
 #pragma unroll
-            for (int bg = 0; bg < NBG; ++bg) {
-                bf16x8 U[CPW][NTU];
-                bf16x8 XB[CPW][DM][2];
-                f32x4 Y[CPW][2], Sr[CPW][DM], Si[CPW][DM];
+            for (int ia = 0; ia < KTX; ++ia)
 #pragma unroll
-                for (int k = 0; k < CPW; ++k) {
-                    load_u(k, bg, U[k], ub);
-                    if constexpr (MODE != kSegState) split_x(X[k][bg], XB[k]);
-                    Y[k][0] = Y[k][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+                for (int ju = 0; ju < NTU; ++ju) {
 #pragma unroll
-                    for (int q = 0; q < DM; ++q) Sr[k][q] = Si[k][q] = f32x4{0.f, 0.f, 0.f, 0.f};
-                }
+                    for (int k = 0; k < CPW; ++k) {
+                        if constexpr (MODE != kSegState) {
+                            if (ia + ju < KT) {
 #pragma unroll
-                for (int ia = 0; ia < KTX; ++ia)
-#pragma unroll
-                    for (int ju = 0; ju < NTU; ++ju) {
-#pragma unroll
-                        for (int k = 0; k < CPW; ++k) {
-                            if constexpr (MODE != kSegState) {
-                                if (ia + ju < KT) {
-#pragma unroll
-                                    for (int mt = 0; mt < 2; ++mt)
-                                        Y[k][mt] = mfma(A[k][2 * DM + mt][ia], U[k][ju], Y[k][mt]);
-                                }
+                                for (int mt = 0; mt < 2; ++mt)
+                                    Y[k][mt] = mfma(A[k][2 * DM + mt][ia], U[k][ju], Y[k][mt]);
                             }
-                            if (ia + ju < KTP) {
+                        }
+                        if (ia + ju < KTP) {
 #pragma unroll
-                                for (int q = 0; q < DM; ++q) {
-                                    Sr[k][q] = mfma(A[k][q][ia], U[k][ju], Sr[k][q]);
-                                    Si[k][q] = mfma(A[k][DM + q][ia], U[k][ju], Si[k][q]);
-                                }
+                            for (int q = 0; q < DM; ++q) {
+                                Sr[k][q] = mfma(A[k][q][ia], U[k][ju], Sr[k][q]);
+                                Si[k][q] = mfma(A[k][DM + q][ia], U[k][ju], Si[k][q]);
                             }
                         }
                     }
-                if constexpr (MODE != kSegState) {
-#pragma unroll
-                    for (int p = 0; p < kWX; ++p)
-#pragma unroll
-                        for (int q = 0; q < DM; ++q)
-#pragma unroll
-                            for (int k = 0; k < CPW; ++k)
-#pragma unroll
-                                for (int mt = 0; mt < 2; ++mt)
-                                    Y[k][mt] = mfma(A[k][2 * DM + 2 + mt * DM + q][kWXa[p]],
-                                                    XB[k][q][kWXx[p]], Y[k][mt]);
                 }
+            if constexpr (MODE != kSegState) {
 #pragma unroll
-                for (int k = 0; k < CPW; ++k)
+                for (int p = 0; p < kWX; ++p)
 #pragma unroll
                     for (int q = 0; q < DM; ++q)
 #pragma unroll
-                        for (int i = 0; i < 4; ++i) {  // carry: X <- lambda^C X + S
-                            const float2 l = lcs[w * CPW + k][g][4 * q + i];
-                            const float xr = X[k][bg][q][i], xi = X[k][bg][DM + q][i];
-                            X[k][bg][q][i] = fmaf(l.x, xr, fmaf(-l.y, xi, Sr[k][q][i]));
-                            X[k][bg][DM + q][i] = fmaf(l.x, xi, fmaf(l.y, xr, Si[k][q][i]));
-                        }
-                if constexpr (MODE != kSegState) stage_y(bg, Y, ys);
+                        for (int k = 0; k < CPW; ++k)
+#pragma unroll
+                            for (int mt = 0; mt < 2; ++mt)
+                                Y[k][mt] = mfma(A[k][2 * DM + 2 + mt * DM + q][kWXa[p]],
+                                                XB[k][q][kWXx[p]], Y[k][mt]);
             }
+#pragma unroll
+            for (int k = 0; k < CPW; ++k)
+#pragma unroll
+                for (int q = 0; q < DM; ++q)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {  // carry: X <- lambda^C X + S
+                        const float2 l = lcs[w * CPW + k][g][4 * q + i];
+                        const float xr = X[k][bg][q][i], xi = X[k][bg][DM + q][i];
+                        X[k][bg][q][i] = fmaf(l.x, xr, fmaf(-l.y, xi, Sr[k][q][i]));
+                        X[k][bg][DM + q][i] = fmaf(l.x, xi, fmaf(l.y, xr, Si[k][q][i]));
+                    }
+            if constexpr (MODE != kSegState) stage_y(bg, Y, ys);
         }
     };
 
@@ -734,30 +630,24 @@ __global__ __launch_bounds__(64 * waves_of(DM)) void mfma_prefill_kernel(
             f32x4 Y[CPW][2];
 #pragma unroll
             for (int k = 0; k < CPW; ++k) {
-                if constexpr (k32) {
-                    float U[8];
-                    load_u32(k, bg, U, ub);
-                    y32(k, U, X[k][bg], Y[k]);
-                } else {
-                    bf16x8 U[NTU];
-                    bf16x8 XB[DM][2];
-                    load_u(k, bg, U, ub);
-                    split_x(X[k][bg], XB);
+                bf16x8 U[NTU];
+                bf16x8 XB[DM][2];
+                load_u(k, bg, U, ub);
+                split_x(X[k][bg], XB);
 #pragma unroll
-                    for (int mt = 0; mt < 2; ++mt) {
-                        Y[k][mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+                for (int mt = 0; mt < 2; ++mt) {
+                    Y[k][mt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-                        for (int ia = 0; ia < KT; ++ia)
+                    for (int ia = 0; ia < KT; ++ia)
 #pragma unroll
-                            for (int ju = 0; ju < NTU; ++ju)
-                                if (ia + ju < KT) Y[k][mt] = mfma(A[k][2 * DM + mt][ia], U[ju], Y[k][mt]);
+                        for (int ju = 0; ju < NTU; ++ju)
+                            if (ia + ju < KT) Y[k][mt] = mfma(A[k][2 * DM + mt][ia], U[ju], Y[k][mt]);
 #pragma unroll
-                        for (int p = 0; p < kWX; ++p)
+                    for (int p = 0; p < kWX; ++p)
 #pragma unroll
-                            for (int q = 0; q < DM; ++q)
-                                Y[k][mt] = mfma(A[k][2 * DM + 2 + mt * DM + q][kWXa[p]],
-                                                XB[q][kWXx[p]], Y[k][mt]);
-                    }
+                        for (int q = 0; q < DM; ++q)
+                            Y[k][mt] = mfma(A[k][2 * DM + 2 + mt * DM + q][kWXa[p]],
+                                            XB[q][kWXx[p]], Y[k][mt]);
                 }
             }
             stage_y(bg, Y, ys);
@@ -898,11 +788,10 @@ __global__ __launch_bounds__(64 * waves_of(DM)) void mfma_prefill_kernel(
 }
 
 // batch groups of 16 rows per wave: two when there are more than 16 rows and
-// the registers allow (float32 inputs with d = 16, one channel per wave; d =
-// 64, whose waves have a SIMD's registers to themselves)
+// the registers allow (float32 inputs with d = 16, one channel per wave)
 int mfma_nbg(int64_t B, int64_t d, bool bf16_io)
 {
-    return ((d == 16 && !bf16_io) || d == 64) && B > kN ? 2 : 1;
+    return d == 16 && !bf16_io && B > kN ? 2 : 1;
 }
 
 template <typename IO, int DM, int NBG, int MODE>
@@ -939,12 +828,10 @@ hipError_t launch_mode(const float2* lam, const void* u, bool bf16_io, int64_t B
     // rows of the MFMA columns: batch rows or (batch row, segment) pairs
     const int64_t rows = MODE == kWhole ? B : MODE == kSegState ? B * (nseg - 1) : B * nseg;
     const bool two = mfma_nbg(rows, d, bf16_io) == 2;
-    if (DM == 4) {  // float32 u/y only (mfma_supported)
+    if (DM == 4) {  // float32 u/y only (mfma_supported), one batch group per wave
         if (bf16_io) return hipErrorInvalidValue;
-        return two ? launch_main<float, 4, 2, MODE>(lam, u, y, state, frag, lamc, B, D, T, nseg,
-                                                    seg_len, xs, stream)
-                   : launch_main<float, 4, 1, MODE>(lam, u, y, state, frag, lamc, B, D, T, nseg,
-                                                    seg_len, xs, stream);
+        return launch_main<float, 4, 1, MODE>(lam, u, y, state, frag, lamc, B, D, T, nseg,
+                                              seg_len, xs, stream);
     }
     if (bf16_io)
         return DM == 2 ? launch_main<bf16, 2, 1, MODE>(lam, u, y, state, frag, lamc, B, D, T,

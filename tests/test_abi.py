@@ -75,9 +75,9 @@ def test_workspace_sizes():
     nch = -(-T // C)
     pow_bytes = -(-(D * d * 8) // 256) * 256
     assert lh.workspace_bytes(B, D, d, T, plan=C) == pow_bytes + B * nch * D * d * 8
-    # automatic plans: matrix-core tables for d = 16 / 32 with D % 8 == 0
-    # (bfloat16 fragments of P, T, W: (4 d/16 + 2) x 3 x 64 x 16 B per channel, plus
-    # lambda^C), the VALU plan otherwise (one pass for the wide d = 64 workload)
+    # automatic plans: matrix-core tables for d = 16 / 32 with D % 8 == 0 and
+    # d = 64 with D % 4 == 0 (bfloat16 fragments of P, T, W: (4 d/16 + 2) x 3 x
+    # 64 x 16 B per channel, plus lambda^C), the VALU plan otherwise
     frag = lambda D, d: D * (4 * (d // 16) + 2) * 3 * 64 * 16  # noqa: E731
     assert lh.workspace_bytes(64, 2048, 16, 4096) == -(-frag(2048, 16) // 256) * 256 + 2048 * 16 * 8
     # the explicit matrix-core plan needs the same tables
@@ -98,12 +98,11 @@ def test_workspace_sizes():
     assert lh.lib().lh_prefill_with_plan_workspace_bytes(2, 12, 16, 64, -1) == bad
     assert lh.lib().lh_prefill_with_plan_workspace_bytes(2, 18, 64, 64, -1) == bad
     assert lh.lib().lh_prefill_with_plan_workspace_bytes(2, 8, 48, 64, -1) == bad
-    # d = 64: float32 blocks of P, T, W (64 + 16 + 64 blocks of 64 lanes x 4 B per
-    # channel), then lambda^C
-    assert lh.workspace_bytes(2, 12, 64, 64, plan=-1) == up(12 * 144 * 64 * 4) + 12 * 64 * 8
-    # the wide d = 64 workload: the matrix-core plan with float32 blocks; with
-    # bfloat16 u/y (no matrix-core plan at d = 64) one VALU pass
-    assert lh.workspace_bytes(256, 2048, 64, 1024) == up(2048 * 144 * 64 * 4) + 2048 * 64 * 8
+    # d = 64: the same fragments (18 per channel), then lambda^C
+    assert lh.workspace_bytes(2, 12, 64, 64, plan=-1) == up(frag(12, 64)) + 12 * 64 * 8
+    # the wide d = 64 workload: the matrix-core plan; with bfloat16 u/y (no
+    # matrix-core plan at d = 64) one VALU pass
+    assert lh.workspace_bytes(256, 2048, 64, 1024) == up(frag(2048, 64)) + 2048 * 64 * 8
     assert lh.prefill_plan(256, 2048, 64, 1024, io="bf16") == "scan"
     # D % 8 != 0: VALU plan, few rows -> 5 chunks of 64 steps
     assert lh.workspace_bytes(2, 70, 16, 300) == 70 * 16 * 8 + 2 * 5 * 70 * 16 * 8
@@ -125,7 +124,7 @@ def test_prefill_plan_query():
     """lh_prefill_plan: the plan lh_prefill takes (host only, no device)."""
     P = lh.prefill_plan
     assert P(1, 4, 4, 64) == "scan"                    # d = 4: no matrix-core plan
-    assert P(256, 2048, 64, 1024) == "mfma"            # d = 64: float32 matrix-core plan
+    assert P(256, 2048, 64, 1024) == "mfma"            # d = 64: matrix-core plan, float32 u/y
     assert P(256, 2048, 64, 1024, io="bf16") == "scan"  # d = 64 needs float32 u/y
     assert P(1, 768, 64, 1024) == "scan"               # d = 64, B T <= 1024
     assert P(4, 768, 64, 1024) == "mfma_seg"           # d = 64, few rows
@@ -456,7 +455,7 @@ def test_noalloc_rejects_sizes_beyond_its_scratch_before_any_device_work():
     L = lh.lib()
     args = auto_args()
     noalloc = args[:11] + [args[-1]]  # no workspace arguments
-    big = dict(B=256, D=2048, d=64, T=1024)  # float32 matrix-core tables: 75.5 MB
+    big = dict(B=256, D=2048, d=64, T=1024)  # matrix-core tables: 114 MB
     assert lh.workspace_bytes(256, 2048, 64, 1024) > lh.NOALLOC_SCRATCH_BYTES
     a = auto_args(**big)
     assert L.lh_prefill_noalloc(*(a[:11] + [a[-1]])) == 5

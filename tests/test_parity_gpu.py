@@ -101,7 +101,7 @@ SMALL = [
     (40, 16, 16, 1024, 3, "f32", -2),  # 2 column groups per wave (float32, d = 16)
     (2, 24, 16, 576, 3, "bf16", -2),   # two segments of 9 chunks (odd count), bfloat16
     (2, 24, 32, 576, 3, "f32", -2),    # the same with float32, d = 32
-    # d = 64: float32 operands, 4 channels per workgroup
+    # d = 64: 4 channels per workgroup, one group of 16 rows per wave
     (2, 12, 64, 96, 3, "f32", -1),     # three channel groups, three full chunks
     (20, 8, 64, 70, 3, "f32", -1),     # second batch group of 4 rows; 70 = 2*32 + 6
     (1, 4, 64, 20, 2, "f32", -1),      # only a partial chunk

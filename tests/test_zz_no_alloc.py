@@ -72,7 +72,7 @@ def test_noalloc_refuses_sizes_beyond_its_scratch():
 
     import paper_2310_18780_amd as lh
 
-    B, D, d, T = 16, 4096, 64, 128  # float32 matrix-core tables of 4096 channels: 153 MB
+    B, D, d, T = 16, 4096, 64, 128  # matrix-core tables of 4096 channels: 229 MB
     assert lh.workspace_bytes(B, D, d, T) > lh.NOALLOC_SCRATCH_BYTES
     lam = torch.zeros((D, d), dtype=torch.complex64, device="cuda")
     h0 = torch.zeros((D,), dtype=torch.float32, device="cuda")
