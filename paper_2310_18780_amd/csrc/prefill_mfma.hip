@@ -224,11 +224,11 @@ __global__ __launch_bounds__(256) void mfma_setup_kernel(const float2* __restric
 // rows; a workgroup of 8 waves owns CW = 8 CPW consecutive channels, so that
 // one (row, step) of its inputs or outputs is a CW-channel segment of a
 // 128-byte line.  Lines of u and y are shared by the workgroups of
-// neighbouring channel groups, and the partial-line traffic, not the
-// arithmetic, bounds the kernel: two channels per wave (32-byte segments for
-// bfloat16) cut it by about a sixth against one (16-byte segments).  A wider
-// segment would need the A operands of more channels than the register file
-// holds next to the carried states.
+// neighbouring channel groups, and the data movement, not the arithmetic,
+// bounds the kernel: two channels per wave (32-byte segments for bfloat16)
+// cut it by about a sixth against one (16-byte segments); 32 channels per
+// workgroup, measured with the arithmetic left out, move the data no faster
+// than 16 (and their A operands would not fit the registers).
 template <typename IO, int DM>
 struct Tiling;
 template <>
@@ -302,7 +302,8 @@ constexpr int cpw_of()
 
 // Chunk tiles of u in flight while a chunk is computed (in registers, one
 // per tile): two where the registers allow it without spilling (all but the
-// state-only pass and the float32 d = 32 whole-prompt kernel).  There are
+// state-only pass and the float32 d = 32 whole-prompt kernel), except at
+// d = 64, where a second tile gained 1%.  There are
 // only two waves per SIMD, both of one workgroup and meeting at its barrier
 // every chunk, so with one tile in flight each chunk waits out most of a
 // memory latency; a second tile hides it.
