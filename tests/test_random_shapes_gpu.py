@@ -24,7 +24,8 @@ def _log(msg):
 
 def _cases(n=48, seed=2026):
     """Every other case has a shape the matrix-core plans take (d = 16 or 32,
-    D a multiple of 8, prompts that split into segments)."""
+    D a multiple of 8, prompts that split into segments); eight more take
+    d = 64 with float32 u/y and D a multiple of 4."""
     rng = np.random.default_rng(seed)
     out = []
     for i in range(n):
@@ -41,6 +42,13 @@ def _cases(n=48, seed=2026):
         io = "bf16" if rng.random() < 0.4 else "f32"
         r_lo = float(rng.choice([0.3, 0.8, 0.99]))
         out.append((i, B, D, d, T, K, io, r_lo))
+    for j in range(8):  # d = 64 on the matrix-core plans: float32 u/y, D % 4 == 0
+        D = int(rng.choice([4, 8, 12, 20, 36, 68]))
+        T = int(rng.choice([1, 31, 33, 96, 257, 512, 576]))
+        B = int(rng.integers(1, 21))
+        K = int(rng.integers(1, 5))
+        r_lo = float(rng.choice([0.3, 0.8, 0.99]))
+        out.append((n + j, B, D, 64, T, K, "f32", r_lo))
     return out
 
 
