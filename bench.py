@@ -8,9 +8,9 @@ Inputs are resident in HBM before the timed region starts.
 
 Prints ONE JSON line: decode tokens/s (B * K / decode time) as ``value``,
 prefill tokens/s, the decode kernel's roofline (HBM) and the prefill's (HBM
-for the matrix-core plans, the VALU peak for the VALU scan; the declared
-flop rate beside it), and the CPU oracle timed on a bounded sample of the
-same workload.
+for the matrix-core plans at d = 16 and 32, the bfloat16 MFMA peak at d = 64,
+the VALU peak for the VALU scan; the declared flop rate beside it), and the
+CPU oracle timed on a bounded sample of the same workload.
 
     python bench.py [--steps K] [--warmup W] [--workload c3]
 """
