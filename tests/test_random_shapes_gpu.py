@@ -22,7 +22,7 @@ def _log(msg):
     print(msg, file=sys.stderr, flush=True)
 
 
-def _cases(n=48, seed=2026):
+def _cases(n=160, seed=2026):
     """Every other case has a shape the matrix-core plans take (d = 16 or 32,
     D a multiple of 8, prompts that split into segments); eight more take
     d = 64 with float32 u/y and D a multiple of 4."""
