@@ -206,8 +206,8 @@ size_t lh_prefill_with_plan_workspace_bytes(int64_t B, int64_t D, int64_t d, int
  *            it within 7/5 of the segmented plan below (the estimate depends
  *            on the input type, so float32 and bfloat16 calls may take
  *            different plans); at d = 64 also when T does not split into
- *            segments and ceil(D/4) * ceil(B/16) >= 256, and never when
- *            B * T <= 1024 (the VALU scan is faster there);
+ *            segments and B >= 4 or ceil(D/4) * ceil(B/16) >= 256, and never
+ *            when B < 4 and B * T <= 1024 (the VALU scan is faster there);
  *   plan = LH_PREFILL_MFMA_SEG: the segmented matrix-core plan: the prompt is
  *            cut into 2^k segments of T / 2^k steps (a multiple of 32, at
  *            least 256), the fewest whose (batch row, segment) pairs fill the

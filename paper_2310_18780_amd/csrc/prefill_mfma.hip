@@ -921,14 +921,16 @@ bool mfma_preferred(int64_t B, int64_t D, int64_t d, int64_t T, bool bf16_io)
 
 int mfma_auto_plan(int64_t B, int64_t D, int64_t d, int64_t T, bool bf16_io)
 {
-    // d = 64 with at most 1024 (row, step) pairs: the VALU plan's chunked scan
-    // beats both matrix-core plans (measured at D = 768 and 2048)
-    if (d == 64 && B * T <= 1024) return 0;
+    // d = 64 with fewer than 4 rows and at most 1024 (row, step) pairs: the
+    // VALU plan's chunked scan beats both matrix-core plans (measured at D =
+    // 768 and 2048)
+    if (d == 64 && B < 4 && B * T <= 1024) return 0;
     if (mfma_preferred(B, D, d, T, bf16_io)) return 1;
     if (mfma_segments(B, D, d, T) >= 2) return 2;
-    // no segments: at d = 64 the whole prompt still beats the VALU plan once
-    // its workgroups (4 channels x 16 rows) fill the GPU
-    if (d == 64 && (D + 3) / 4 * ((B + kN - 1) / kN) >= kMinWorkgroups) return 1;
+    // no segments: at d = 64 the whole prompt beats the VALU plan from 4 rows
+    // on (D = 768, T = 256: 0.058 ms against 0.067 ms at 4 rows, 0.13 ms at
+    // 16), or once its workgroups (4 channels x 16 rows) fill the GPU
+    if (d == 64 && (B >= 4 || (D + 3) / 4 * ((B + kN - 1) / kN) >= kMinWorkgroups)) return 1;
     return 0;
 }
 

@@ -126,9 +126,11 @@ def test_prefill_plan_query():
     assert P(1, 4, 4, 64) == "scan"                    # d = 4: no matrix-core plan
     assert P(256, 2048, 64, 1024) == "mfma"            # d = 64: matrix-core plan, float32 u/y
     assert P(256, 2048, 64, 1024, io="bf16") == "scan"  # d = 64 needs float32 u/y
-    assert P(1, 768, 64, 1024) == "scan"               # d = 64, B T <= 1024
+    assert P(1, 768, 64, 1024) == "scan"               # d = 64, B < 4 and B T <= 1024
     assert P(4, 768, 64, 1024) == "mfma_seg"           # d = 64, few rows
-    assert P(16, 768, 64, 1000) == "scan"              # no segments, 192 workgroups
+    assert P(16, 768, 64, 1000) == "mfma"              # no segments, 4 rows or more
+    assert P(2, 768, 64, 1000) == "scan"               # no segments, fewer than 4 rows, 192 workgroups
+    assert P(4, 768, 64, 256) == "mfma"                # no segments, 4 rows
     assert P(64, 768, 64, 1000) == "mfma"              # no segments, 768 workgroups
     assert P(64, 2048, 16, 4096, io="bf16") == "mfma"  # enough (channel, row) tiles
     assert P(4, 1024, 32, 65536) == "mfma_seg"         # 4 rows, long prompt
